@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Benchmark of the hot path on one MI355X.
+
+Workload: 4000 rows x 32000 binary32 logits, i.i.d. N(0, 2) from seed 0, with
+1% of the rows shifted by +1000 (the paper's large-batch softmax case).  One
+step is the whole hot path over that batch, resident in HBM:
+
+  1. online softmax (two loads and one store per element), then
+  2. fused online softmax + top-k, K = 5 (one load per element).
+
+The printed JSON line reports the step's algorithmic bytes per second
+(online: 12 B/element; fused top-k: 4 B/element + 8 B per output pair), a
+per-kernel breakdown timed with HIP events on the launch stream, the roofline
+entry of the dominant kernel, and the oracle timed on the host cores.  The
+naive and safe modes are timed on the same batch after the steps, for the
+paper's memory-access comparison.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, decimal GB/s
+N_ROWS, V_LEN, SIGMA, SHIFT_FRAC, K_TOP = 4000, 32000, 2.0, 0.01, 5
+WORKLOAD = "online softmax + fused softmax/top-5, 4000x32000 fp32 N(0,2), 1% rows +1000"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_1805_02867_amd", "csrc", "*"))):
+        with open(p, "rb") as f:
+            h.update(os.path.basename(p).encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_entry(name: str):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    e = data.get(name)
+    if not e or e.get("source_sha") != kernel_source_sha():
+        return None
+    return e.get("bytes_per_launch")
+
+
+def timed_calls(fn, reps: int, stream):
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for a, b in evs:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in evs]  # ms
+
+
+def median(xs):
+    s = sorted(xs)
+    n = len(s)
+    return s[n // 2] if n % 2 else 0.5 * (s[n // 2 - 1] + s[n // 2])
+
+
+def pct(xs, q):
+    s = sorted(xs)
+    return s[min(len(s) - 1, max(0, int(round(q * (len(s) - 1)))))]
+
+
+def copy_probe():
+    """A plain 512 MB device copy, for scaling FETCH_SIZE / WRITE_SIZE."""
+    import torch
+    n = N_ROWS * V_LEN
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    t = timed_calls(lambda: b.copy_(a), 20, torch.cuda.current_stream())
+    log(f"copy {n * 4 / 1e6:.0f} MB: median {median(t) * 1e3:.1f} us, "
+        f"{2 * n * 4 / (median(t) * 1e-3) / 1e9:.0f} GB/s (read+write)")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--compare-reps", type=int, default=20)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(rows shard across GPUs with no communication; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_1805_02867_amd as osm
+    from paper_1805_02867_amd import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    osm.lib()  # fail loudly if the HIP library is not built
+    if args.copy_probe:
+        copy_probe()
+        return
+
+    dev = torch.device("cuda:0")
+    N, V, K = N_ROWS, V_LEN, K_TOP
+    x = synth.logits(N, V, sigma=SIGMA, seed=0, device=dev, shift_frac=SHIFT_FRAC)
+    y = torch.empty_like(x)
+    vals = torch.empty((N, K), dtype=torch.float32, device=dev)
+    idx = torch.empty((N, K), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    plan = osm.plan(N, V, mode="online")
+    log(f"device {torch.cuda.get_device_name(0)}; plan online {plan}")
+
+    def soft():
+        osm.softmax_fwd(x, y, mode="online")
+
+    def topk():
+        osm.softmax_topk(x, K, vals, idx)
+
+    for _ in range(args.warmup):
+        soft()
+        topk()
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` steps, events around every launch
+    ev_s = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(args.steps)]
+    ev_t = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev_s[i][0].record(stream)
+        soft()
+        ev_s[i][1].record(stream)
+        ev_t[i][0].record(stream)
+        topk()
+        ev_t[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_soft = [a.elapsed_time(b) for a, b in ev_s]
+    ms_topk = [a.elapsed_time(b) for a, b in ev_t]
+    log(f"{args.steps} steps in {wall:.3f} s")
+
+    bytes_soft = 12.0 * N * V
+    bytes_topk = 4.0 * N * V + 8.0 * N * K
+    step_ms = wall * 1e3 / args.steps
+    value = (bytes_soft + bytes_topk) / (step_ms * 1e-3) / 1e9
+    avg_soft = sum(ms_soft) / len(ms_soft)
+    avg_topk = sum(ms_topk) / len(ms_topk)
+    gbs_soft = bytes_soft / (avg_soft * 1e-3) / 1e9
+    gbs_topk = bytes_topk / (avg_topk * 1e-3) / 1e9
+
+    # the paper's comparison: naive and safe on the same batch
+    compare = {}
+    for mode, nbytes in (("naive", 12.0), ("safe", 16.0), ("online", 12.0)):
+        t = timed_calls(lambda m=mode: osm.softmax_fwd(x, y, mode=m), args.compare_reps, stream)
+        compare[mode] = {"median_us": round(median(t) * 1e3, 2),
+                         "p10_us": round(pct(t, 0.1) * 1e3, 2),
+                         "p90_us": round(pct(t, 0.9) * 1e3, 2),
+                         "algorithmic_GBps": round(nbytes * N * V / (median(t) * 1e-3) / 1e9, 1)}
+    ratio = compare["safe"]["median_us"] / compare["online"]["median_us"]
+    separated = compare["safe"]["p10_us"] > compare["online"]["p90_us"]
+
+    traffic = traffic_entry("softmax_online_4000x32000_f32")
+    roofline = {"bound": "hbm", "achieved": round(gbs_soft, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(gbs_soft / PEAK_HBM_GBS, 4),
+                "traffic": traffic}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        rows = 1000
+        xh = x[:rows].cpu().numpy()
+        oracle.softmax(xh[:8])  # load the library outside the timing
+        t1 = time.perf_counter()
+        oracle.softmax(xh)
+        oracle.topk(xh, K)
+        dt = time.perf_counter() - t1
+        cpu_bytes = rows * V * 12.0 + rows * V * 4.0 + rows * K * 8.0
+        cpu = {"value": round(cpu_bytes / dt / 1e9, 3), "unit": "GB/s",
+               "cores": oracle.threads(), "kind": "oracle",
+               "sample": f"first {rows} of the {N} rows, one step (softmax + top-5), "
+                         f"{dt:.2f} s wall"}
+        log(f"oracle: {dt:.2f} s for {rows} rows on {oracle.threads()} threads")
+
+    out = {
+        "metric": "achieved HBM GB/s (% of peak) for online softmax + fused softmax+top-K rows/s",
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD, "N": N, "V": V, "K": K, "global_batch": N,
+                   "parallelism": "none (1 GPU)"},
+        "online_softmax": {"avg_us": round(avg_soft * 1e3, 2), "GBps": round(gbs_soft, 1),
+                           "frac_of_peak": round(gbs_soft / PEAK_HBM_GBS, 4),
+                           "rows_per_s": round(N / (avg_soft * 1e-3), 1),
+                           "kernel_plan": list(plan)},
+        "fused_topk": {"avg_us": round(avg_topk * 1e3, 2), "GBps": round(gbs_topk, 1),
+                       "frac_of_peak": round(gbs_topk / PEAK_HBM_GBS, 4),
+                       "rows_per_s": round(N / (avg_topk * 1e-3), 1)},
+        "modes": compare,
+        "safe_over_online": round(ratio, 3),
+        "online_faster_than_safe_p10_p90_separated": bool(separated),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

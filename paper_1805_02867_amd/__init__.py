@@ -1,0 +1,152 @@
+"""Python binding of libosoftmax (online-normalizer softmax and fused softmax +
+top-k on MI355X).  Argument marshalling only: every step of the computation
+runs in the library's HIP kernels, reached through its C ABI
+(``include/osoftmax.h``).  PyTorch supplies device memory and the current
+stream.  There is no fallback: if the library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libosoftmax.so")
+
+F32, BF16 = 0, 1
+NAIVE, SAFE, ONLINE = 0, 1, 2
+KERNEL_AUTO, KERNEL_ROWS, KERNEL_SPLIT = 0, 1, 2
+OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM = 0, 1, 2, 3, 4
+TOPK_KMAX = 64
+
+MODES = {"naive": NAIVE, "safe": SAFE, "online": ONLINE}
+_DTYPES = {torch.float32: F32, torch.bfloat16: BF16}
+
+_lib = None
+
+
+class OsmError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded C library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                           "(or python paper_1805_02867_amd/build.py)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    L.softmax_fwd.argtypes = [vp, vp, i64, i64, i32, i32, vp]
+    L.softmax_fwd.restype = i32
+    L.softmax_fwd_ex.argtypes = [vp, vp, i64, i64, i32, i32, i32, i64, vp]
+    L.softmax_fwd_ex.restype = i32
+    L.softmax_topk.argtypes = [vp, vp, vp, i64, i64, i32, vp]
+    L.softmax_topk.restype = i32
+    L.softmax_topk_dt.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
+    L.softmax_topk_dt.restype = i32
+    L.osm_plan.argtypes = [i64, i64, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i64)]
+    L.osm_plan.restype = i32
+    L.osm_status_string.argtypes = [i32]
+    L.osm_status_string.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return lib().osm_status_string(int(status)).decode()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _batch(x: torch.Tensor, name: str = "x"):
+    if not isinstance(x, torch.Tensor) or not x.is_cuda:
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if x.dtype not in _DTYPES:
+        raise ValueError(f"{name} must be float32 or bfloat16, got {x.dtype}")
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if x.dim() == 1:
+        return 1, x.shape[0]
+    if x.dim() != 2:
+        raise ValueError(f"{name} must be 1-D or 2-D (N x V)")
+    return x.shape[0], x.shape[1]
+
+
+def _mode(mode) -> int:
+    if isinstance(mode, str):
+        if mode not in MODES:
+            raise ValueError(f"mode must be one of {sorted(MODES)}")
+        return MODES[mode]
+    return int(mode)
+
+
+def softmax_fwd(x: torch.Tensor, y: torch.Tensor | None = None, mode="online",
+                stream=None, kernel: int = KERNEL_AUTO, param: int = 0) -> torch.Tensor:
+    """y = Softmax(x) per row via ``softmax_fwd`` / ``softmax_fwd_ex``."""
+    N, V = _batch(x)
+    if y is None:
+        y = torch.empty_like(x)
+    else:
+        Ny, Vy = _batch(y, "y")
+        if (Ny, Vy) != (N, V) or y.dtype != x.dtype or y.device != x.device:
+            raise ValueError("y must match x in shape, dtype and device")
+    dt = _DTYPES[x.dtype]
+    if kernel == KERNEL_AUTO:
+        rc = lib().softmax_fwd(x.data_ptr(), y.data_ptr(), N, V, dt, _mode(mode),
+                               _stream(stream))
+    else:
+        rc = lib().softmax_fwd_ex(x.data_ptr(), y.data_ptr(), N, V, dt, _mode(mode),
+                                  int(kernel), int(param), _stream(stream))
+    if rc != OK:
+        raise OsmError(rc, "softmax_fwd")
+    return y
+
+
+def softmax_topk(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,
+                 idx: torch.Tensor | None = None, stream=None):
+    """(vals, idx) = fused softmax + top-k per row via ``softmax_topk``
+    (binary32 rows) or ``softmax_topk_dt`` (bfloat16 rows)."""
+    N, V = _batch(x)
+    if vals is None:
+        vals = torch.empty((N, K), dtype=torch.float32, device=x.device)
+    if idx is None:
+        idx = torch.empty((N, K), dtype=torch.int32, device=x.device)
+    for t, dt, nm in ((vals, torch.float32, "vals"), (idx, torch.int32, "idx")):
+        if (t.dtype != dt or not t.is_contiguous() or t.numel() != N * K
+                or t.device != x.device):
+            raise ValueError(f"{nm} must be a contiguous {dt} tensor of N*K elements on x's device")
+    if x.dtype == torch.float32:
+        rc = lib().softmax_topk(x.data_ptr(), vals.data_ptr(), idx.data_ptr(), N, V, int(K),
+                                _stream(stream))
+    else:
+        rc = lib().softmax_topk_dt(x.data_ptr(), vals.data_ptr(), idx.data_ptr(), N, V,
+                                   int(K), _DTYPES[x.dtype], _stream(stream))
+    if rc != OK:
+        raise OsmError(rc, "softmax_topk")
+    return vals, idx
+
+
+softmax_topk_dt = softmax_topk
+
+
+def plan(N: int, V: int, dtype=torch.float32, mode="online"):
+    """(kernel, param) that softmax_fwd uses for this shape (``osm_plan``)."""
+    k = ctypes.c_int()
+    p = ctypes.c_int64()
+    dt = _DTYPES[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    rc = lib().osm_plan(int(N), int(V), dt, _mode(mode), ctypes.byref(k), ctypes.byref(p))
+    if rc != OK:
+        raise OsmError(rc, "osm_plan")
+    return k.value, p.value

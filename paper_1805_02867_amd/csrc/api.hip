@@ -1,0 +1,218 @@
+// C-ABI of the library: argument validation, kernel choice and launches.
+// Declarations and the contract of every entry point are in osoftmax.h.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <mutex>
+
+#include "kernels.h"
+#include "osoftmax.h"
+
+namespace {
+
+constexpr int64_t kMaxDim = 2147483647;  // 2^31 - 1
+constexpr int kMaxDevices = 64;
+
+size_t elem_size(int dtype) { return dtype == OSM_BF16 ? 2 : 4; }
+int elems_per_vec(int dtype) { return dtype == OSM_BF16 ? 8 : 4; }
+
+// ------------------------------------------------------------ device state
+struct DeviceState {
+    std::once_flag once;
+    int cus = 0;
+    hipMemPool_t pool = nullptr;
+    bool pool_ok = false;
+};
+DeviceState g_dev[kMaxDevices];
+
+DeviceState* device_state(int* dev_out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    DeviceState& s = g_dev[dev];
+    std::call_once(s.once, [&s, dev]() {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+        s.cus = cus;
+        // A library-owned stream-ordered pool keeps split-V scratch cheap to
+        // allocate and free on any stream without touching the device's
+        // default pool settings.
+        hipMemPoolProps props = {};
+        props.allocType = hipMemAllocationTypePinned;
+        props.handleTypes = hipMemHandleTypeNone;
+        props.location.type = hipMemLocationTypeDevice;
+        props.location.id = dev;
+        if (hipMemPoolCreate(&s.pool, &props) == hipSuccess) {
+            uint64_t keep = UINT64_MAX;
+            (void)hipMemPoolSetAttribute(s.pool, hipMemPoolAttrReleaseThreshold, &keep);
+            s.pool_ok = true;
+        }
+        (void)hipGetLastError();
+    });
+    if (dev_out) *dev_out = dev;
+    return &s;
+}
+
+// ------------------------------------------------------------- validation
+bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
+    uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Sizes, dtype and byte count of an N x V batch; false on any violation.
+bool check_shape(int64_t N, int64_t V, int dtype, size_t* bytes) {
+    if (N < 0 || N > kMaxDim || V < 1 || V > kMaxDim) return false;
+    if (dtype != OSM_F32 && dtype != OSM_BF16) return false;
+    // N, V < 2^31 and element size <= 4: the product is below 2^64
+    *bytes = (size_t)N * (size_t)V * elem_size(dtype);
+    return true;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? OSM_OK : OSM_EHIP; }
+
+// ---------------------------------------------------------------- planning
+struct Plan {
+    int kernel;
+    int64_t param;
+};
+
+Plan choose(int64_t N, int64_t V, int dtype, int cus) {
+    const int64_t E = elems_per_vec(dtype);
+    const int64_t nv = (V + E - 1) / E;  // 16-byte vectors per row
+    // Short rows: a lane group per row, sized so each lane has ~2-4 vectors.
+    if (nv <= 16) return {OSM_KERNEL_ROWS, 4};
+    if (nv <= 32) return {OSM_KERNEL_ROWS, 8};
+    if (nv <= 64) return {OSM_KERNEL_ROWS, 16};
+    if (nv <= 128) return {OSM_KERNEL_ROWS, 32};
+    if (nv <= 1024) return {OSM_KERNEL_ROWS, 64};
+    // Long rows but too few of them to fill the chip: split each row.
+    const int64_t want_blocks = 4 * (int64_t)cus;
+    if (N < 2 * (int64_t)cus && V >= 16384) {
+        int64_t S = (want_blocks + N - 1) / N;
+        int64_t s_cap = (V + 4095) / 4096;  // keep chunks >= 4096 elements
+        if (S > s_cap) S = s_cap;
+        if (S >= 2) return {OSM_KERNEL_SPLIT, S};
+    }
+    if (nv <= 2048) return {OSM_KERNEL_ROWS, 256};
+    if (nv <= 8192) return {OSM_KERNEL_ROWS, 512};
+    return {OSM_KERNEL_ROWS, 1024};
+}
+
+bool team_ok(int64_t t) {
+    return t == 4 || t == 8 || t == 16 || t == 32 || t == 64 || t == 128 || t == 256 ||
+           t == 512 || t == 1024;
+}
+
+int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mode, int kernel,
+                int64_t param, hipStream_t stream) {
+    size_t bytes = 0;
+    if (!check_shape(N, V, dtype, &bytes)) return OSM_EINVAL;
+    if (mode != OSM_NAIVE && mode != OSM_SAFE && mode != OSM_ONLINE) return OSM_EINVAL;
+    if (kernel != OSM_KERNEL_AUTO && kernel != OSM_KERNEL_ROWS && kernel != OSM_KERNEL_SPLIT)
+        return OSM_EINVAL;
+    if (kernel == OSM_KERNEL_ROWS && !team_ok(param)) return OSM_EINVAL;
+    if (kernel == OSM_KERNEL_SPLIT && (param < 1 || param > kMaxDim)) return OSM_EINVAL;
+    if (N == 0) return OSM_OK;
+    if (!x || !y) return OSM_EINVAL;
+    const size_t es = elem_size(dtype);
+    if (!aligned(x, es) || !aligned(y, es)) return OSM_EINVAL;
+    if (overlaps(x, bytes, y, bytes)) return OSM_EINVAL;
+    const bool vec = (((uintptr_t)x - (uintptr_t)y) % 16) == 0;
+
+    int dev = 0;
+    DeviceState* ds = device_state(&dev);
+    if (!ds) return OSM_EHIP;
+    Plan p = kernel == OSM_KERNEL_AUTO ? choose(N, V, dtype, ds->cus) : Plan{kernel, param};
+
+    if (p.kernel == OSM_KERNEL_ROWS)
+        return hip_status(osm::launch_softmax_rows(x, y, N, V, dtype, mode, (int)p.param, vec,
+                                                   stream));
+
+    // split-V: chunk = ceil(V / S) rounded up to whole 16-byte vectors
+    const int64_t E = elems_per_vec(dtype);
+    int64_t S = p.param;
+    if (S > V) S = V;
+    int64_t chunk = (V + S - 1) / S;
+    chunk = (chunk + E - 1) / E * E;
+    S = (V + chunk - 1) / chunk;  // drop chunks that would start past the row
+    if (N * S > kMaxDim) return OSM_EINVAL;
+    if (!ds->pool_ok) return OSM_ENOMEM;
+    void* scratch = nullptr;
+    const size_t sbytes = (size_t)N * (size_t)S * 8;
+    if (hipMallocFromPoolAsync(&scratch, sbytes, ds->pool, stream) != hipSuccess || !scratch) {
+        (void)hipGetLastError();
+        return OSM_ENOMEM;
+    }
+    hipError_t e = osm::launch_softmax_split(x, y, scratch, N, V, dtype, mode, S, chunk, vec,
+                                             stream);
+    hipError_t f = hipFreeAsync(scratch, stream);
+    if (e != hipSuccess) return OSM_EHIP;
+    return hip_status(f);
+}
+
+int run_topk(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K, int dtype,
+             hipStream_t stream) {
+    size_t bytes = 0;
+    if (!check_shape(N, V, dtype, &bytes)) return OSM_EINVAL;
+    if (K < 1 || K > OSM_TOPK_KMAX || (int64_t)K > V) return OSM_EINVAL;
+    if (N == 0) return OSM_OK;
+    if (!x || !vals || !idx) return OSM_EINVAL;
+    if (!aligned(x, elem_size(dtype)) || !aligned(vals, 4) || !aligned(idx, 4)) return OSM_EINVAL;
+    const size_t ob = (size_t)N * (size_t)K * 4;
+    if (overlaps(x, bytes, vals, ob) || overlaps(x, bytes, idx, ob) || overlaps(vals, ob, idx, ob))
+        return OSM_EINVAL;
+    if (!device_state(nullptr)) return OSM_EHIP;
+    return hip_status(osm::launch_topk_fused(x, vals, idx, N, V, K, dtype, true, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int softmax_fwd(const void* x, void* y, int64_t N, int64_t V, int dtype, int mode,
+                hipStream_t stream) {
+    return run_softmax(x, y, N, V, dtype, mode, OSM_KERNEL_AUTO, 0, stream);
+}
+
+int softmax_fwd_ex(const void* x, void* y, int64_t N, int64_t V, int dtype, int mode, int kernel,
+                   int64_t param, hipStream_t stream) {
+    return run_softmax(x, y, N, V, dtype, mode, kernel, param, stream);
+}
+
+int softmax_topk(const float* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
+                 hipStream_t stream) {
+    return run_topk(x, vals, idx, N, V, K, OSM_F32, stream);
+}
+
+int softmax_topk_dt(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
+                    int dtype, hipStream_t stream) {
+    return run_topk(x, vals, idx, N, V, K, dtype, stream);
+}
+
+int osm_plan(int64_t N, int64_t V, int dtype, int mode, int* kernel, int64_t* param) {
+    size_t bytes = 0;
+    if (!check_shape(N, V, dtype, &bytes)) return OSM_EINVAL;
+    if (mode != OSM_NAIVE && mode != OSM_SAFE && mode != OSM_ONLINE) return OSM_EINVAL;
+    if (!kernel || !param) return OSM_EINVAL;
+    DeviceState* ds = device_state(nullptr);
+    Plan p = choose(N, V, dtype, ds ? ds->cus : 256);
+    *kernel = p.kernel;
+    *param = p.param;
+    return OSM_OK;
+}
+
+const char* osm_status_string(int status) {
+    switch (status) {
+        case OSM_OK: return "success";
+        case OSM_EINVAL: return "invalid argument";
+        case OSM_EUNSUPPORTED: return "unsupported configuration";
+        case OSM_EHIP: return "HIP error while enqueuing work";
+        case OSM_ENOMEM: return "scratch allocation failed";
+        default: return "unknown status";
+    }
+}
+
+}  // extern "C"

@@ -59,7 +59,7 @@ def logits(N: int, V: int, *, sigma: float = 1.0, seed: int = 0,
                 amax = int(torch.argmax(row).item())
                 pos = tie_map[r].clone()
                 pos[pos >= amax] += 1  # skip the arg-max itself
-                row[pos.to(device)] = row[amax]
+                row.index_fill_(0, pos.to(device), row[amax].item())  # exact: f32 -> f64 -> f32
         x[r0:r1].copy_(blk)
     return x
 

@@ -1,0 +1,120 @@
+"""C-ABI contract checks that need no GPU: the library loads, exports every
+function include/osoftmax.h declares, and rejects invalid arguments on the
+host before touching the device (fake, never dereferenced pointers)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1805_02867_amd as osm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "osoftmax.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"OSM_API\s+[\w\s\*]+?\b(\w+)\s*\(", text)
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for want in ("softmax_fwd", "softmax_fwd_ex", "softmax_topk", "softmax_topk_dt",
+                 "osm_plan", "osm_status_string"):
+        assert want in names
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(osm.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_enum_values_match_header():
+    text = open(HEADER).read()
+    for name, val in (("OSM_F32", osm.F32), ("OSM_BF16", osm.BF16), ("OSM_NAIVE", osm.NAIVE),
+                      ("OSM_SAFE", osm.SAFE), ("OSM_ONLINE", osm.ONLINE), ("OSM_OK", osm.OK),
+                      ("OSM_EINVAL", osm.EINVAL), ("OSM_EHIP", osm.EHIP),
+                      ("OSM_ENOMEM", osm.ENOMEM), ("OSM_KERNEL_ROWS", osm.KERNEL_ROWS),
+                      ("OSM_KERNEL_SPLIT", osm.KERNEL_SPLIT)):
+        assert re.search(rf"\b{name}\s*=\s*{val}\b", text), name
+    assert re.search(rf"#define OSM_TOPK_KMAX {osm.TOPK_KMAX}\b", text)
+
+
+def test_status_strings():
+    for s in range(5):
+        assert osm.status_string(s)
+    assert osm.status_string(99) == "unknown status"
+
+
+# Fake device addresses: the validation below must reject these calls before
+# any HIP call, so they are never dereferenced.
+X, Y = 0x10000000, 0x20000000
+
+
+@pytest.mark.parametrize("args", [
+    (X, Y, -1, 10, 0, 2),          # N < 0
+    (X, Y, 4, 0, 0, 2),            # V < 1
+    (X, Y, 4, 1 << 31, 0, 2),      # V too large
+    (X, Y, 1 << 31, 4, 0, 2),      # N too large
+    (X, Y, 4, 10, 2, 2),           # unknown dtype
+    (X, Y, 4, 10, 0, 3),           # unknown mode
+    (0, Y, 4, 10, 0, 2),           # null x
+    (X, 0, 4, 10, 0, 2),           # null y
+    (X, X + 8, 4, 10, 0, 2),       # overlap
+    (X + 2, Y, 4, 10, 0, 2),       # x not aligned to binary32
+    (X, Y + 1, 4, 10, 1, 2),       # y not aligned to bfloat16
+])
+def test_softmax_fwd_rejects(args):
+    assert osm.lib().softmax_fwd(*args, None) == osm.EINVAL
+
+
+def test_n_zero_is_a_noop():
+    assert osm.lib().softmax_fwd(0, 0, 0, 10, 0, 2, None) == osm.OK
+    assert osm.lib().softmax_topk(0, 0, 0, 0, 10, 5, None) == osm.OK
+
+
+@pytest.mark.parametrize("kernel,param", [(7, 0), (1, 3), (1, 2048), (1, 0), (2, 0), (2, -5)])
+def test_softmax_fwd_ex_rejects(kernel, param):
+    assert osm.lib().softmax_fwd_ex(X, Y, 4, 10, 0, 2, kernel, param, None) == osm.EINVAL
+
+
+V_, I_ = 0x30000000, 0x40000000
+
+
+@pytest.mark.parametrize("args", [
+    (X, V_, I_, 4, 10, 0),          # K < 1
+    (X, V_, I_, 4, 10, 11),         # K > V
+    (X, V_, I_, 4, 100, 65),        # K > KMAX
+    (0, V_, I_, 4, 10, 5),          # null x
+    (X, 0, I_, 4, 10, 5),           # null vals
+    (X, V_, 0, 4, 10, 5),           # null idx
+    (X, X + 16, I_, 4, 10, 5),      # vals overlaps x
+    (X, V_, V_ + 8, 4, 10, 5),      # idx overlaps vals
+    (X, V_ + 2, I_, 4, 10, 5),      # misaligned vals
+])
+def test_softmax_topk_rejects(args):
+    assert osm.lib().softmax_topk(*args, None) == osm.EINVAL
+
+
+def test_softmax_topk_dt_rejects_unknown_dtype():
+    assert osm.lib().softmax_topk_dt(X, V_, I_, 4, 10, 5, 7, None) == osm.EINVAL
+
+
+def test_plan_rejects_bad_shapes():
+    k = ctypes.c_int()
+    p = ctypes.c_int64()
+    assert osm.lib().osm_plan(4, 0, 0, 2, ctypes.byref(k), ctypes.byref(p)) == osm.EINVAL
+    assert osm.lib().osm_plan(4, 10, 5, 2, ctypes.byref(k), ctypes.byref(p)) == osm.EINVAL
+    assert osm.lib().osm_plan(4, 10, 0, 9, ctypes.byref(k), ctypes.byref(p)) == osm.EINVAL
+    assert osm.lib().osm_plan(4, 10, 0, 2, None, ctypes.byref(p)) == osm.EINVAL
+
+
+def test_python_binding_refuses_cpu_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        osm.softmax_fwd(torch.zeros(2, 3))
+    with pytest.raises(ValueError):
+        osm.softmax_topk(torch.zeros(2, 3), 1)

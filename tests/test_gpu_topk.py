@@ -1,0 +1,139 @@
+"""GPU parity of the fused softmax + top-k against the binary64 oracle:
+indices bit-exact (ties to the lower index), values within the binary32 rule."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1805_02867_amd as osm
+from paper_1805_02867_amd import synth
+from parity import assert_topk_equal, host_dtype, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need an MI355X; none is visible")
+    return torch.device("cuda:0")
+
+
+def check(x, K, what):
+    vals, idx = osm.softmax_topk(x, K)
+    torch.cuda.synchronize()
+    v64, z64 = oracle.topk(to_host(x), K, host_dtype(x))
+    assert_topk_equal(to_host(vals), to_host(idx), v64, z64, what)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_lengths_and_k(dev, dtype):
+    for V in (1, 2, 3, 5, 8, 9, 63, 64, 65, 255, 256, 257, 1000, 1001, 4097, 32000, 50001):
+        for K in sorted({1, 2, 5, 10, 50, 64, V}):
+            if K > V or K > osm.TOPK_KMAX:
+                continue
+            N = 23 if V < 10000 else 7
+            print(f"topk dtype={dtype} V={V} K={K}", flush=True)
+            x = synth.logits(N, V, sigma=2.0, seed=V * 7 + K, dtype=dtype, device=dev)
+            check(x, K, f"{dtype} V={V} K={K}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_heavy_ties(dev, dtype):
+    """Values on a coarse grid: long runs of equal values straddle slot K."""
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    g = torch.Generator(device=dev).manual_seed(4)
+    for V in (100, 3000, 40000):
+        x = torch.randint(-3, 4, (13, V), generator=g, device=dev).to(tdt) * 0.5
+        for K in (1, 5, 17, 64):
+            check(x, K, f"ties {dtype} V={V} K={K}")
+    # every element equal
+    x = torch.full((5, 5000), 1.25, dtype=tdt, device=dev)
+    check(x, 64, "all equal")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_special_values(dev, dtype):
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    ninf = float("-inf")
+    V = 700
+    base = torch.linspace(-5, 5, V)
+    rows = torch.stack([
+        base,
+        base.flip(0),
+        torch.where(torch.arange(V) % 3 == 0, torch.tensor(ninf), base),  # -inf elements
+        torch.cat([torch.full((V - 3,), ninf), torch.tensor([1.0, 2.0, 3.0])]),  # few finite
+        torch.zeros(V) * torch.where(torch.arange(V) % 2 == 0, 1.0, -1.0),  # +-0.0 ties
+        base + 1000.0,
+    ]).to(tdt).to(dev)
+    for K in (1, 3, 5, 10):
+        check(rows, K, f"special {dtype} K={K}")
+    # K larger than the finite elements: -inf elements fill in, lowest index first
+    check(rows[3:4], 8, f"-inf fill {dtype}")
+
+
+def test_unaligned_rows(dev):
+    """x starting off the 16-byte phase (a view into a larger buffer)."""
+    buf = synth.logits(1, 37 * 999 + 3, sigma=2.0, seed=8, device=dev)
+    x = buf[0, 3:].view(37, 999)
+    check(x, 5, "unaligned x")
+    bbuf = synth.logits(1, 21 * 4097 + 5, sigma=2.0, seed=9, dtype="bf16", device=dev)
+    check(bbuf[0, 5:].view(21, 4097), 7, "unaligned bf16 x")
+
+
+def test_deterministic(dev):
+    x = synth.logits(500, 32000, sigma=2.0, seed=10, device=dev)
+    a = osm.softmax_topk(x, 10)
+    b = osm.softmax_topk(x, 10)
+    torch.cuda.synchronize()
+    assert torch.equal(a[1], b[1]) and torch.equal(a[0].view(torch.int32), b[0].view(torch.int32))
+
+
+def test_small_workload_16x1000(dev):
+    w = synth.WORKLOADS["softmax_topk_16x1000_f32"]
+    x = synth.logits(w["N"], w["V"], sigma=w["sigma"], seed=0, device=dev)
+    check(x, w["K"], "16x1000 K=5")
+
+
+@pytest.mark.slow
+def test_workload_4000x32000_k5(dev):
+    w = synth.WORKLOADS["softmax_4000x32000_f32_shift"]
+    x = synth.logits(w["N"], w["V"], sigma=w["sigma"], seed=0, device=dev,
+                     shift_frac=w["shift_frac"])
+    check(x, 5, "4000x32000 K=5")
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("K", [5, 10])
+def test_workload_4000x50000_ties(dev, K):
+    w = synth.WORKLOADS["topk_4000x50000_f32_ties"]
+    x = synth.logits(w["N"], w["V"], sigma=w["sigma"], seed=0, device=dev,
+                     tie_frac=w["tie_frac"])
+    _, tied = synth.special_rows(w["N"], seed=0, tie_frac=w["tie_frac"])
+    xh = to_host(x)
+    # the tie rows really hold their maximum four times
+    for r in tied[:5]:
+        assert (xh[r] == xh[r].max()).sum() == 4
+    vals, idx = osm.softmax_topk(x, K)
+    torch.cuda.synchronize()
+    v64, z64 = oracle.topk(xh, K)
+    assert_topk_equal(to_host(vals), to_host(idx), v64, z64, f"4000x50000 K={K}")
+    zt = to_host(idx)[tied]
+    for r, z in zip(tied, zt):
+        assert list(z[:4]) == sorted(z[:4]), "tied maxima must come in increasing index order"
+
+
+@pytest.mark.slow
+def test_workload_32768x128256_bf16_k50_sampled(dev):
+    w = synth.WORKLOADS["softmax_topk_32768x128256_bf16"]
+    x = synth.logits(w["N"], w["V"], sigma=w["sigma"], seed=0, dtype="bf16", device=dev)
+    vals, idx = osm.softmax_topk(x, w["K"])
+    torch.cuda.synchronize()
+    g = torch.Generator().manual_seed(321)
+    rows = torch.cat([torch.tensor([0, w["N"] - 1]),
+                      torch.randperm(w["N"], generator=g)[:1024]])
+    rr = rows.to(dev)
+    xh = to_host(x.index_select(0, rr))
+    v64, z64 = oracle.topk(xh, w["K"], "bf16")
+    assert_topk_equal(to_host(vals.index_select(0, rr)), to_host(idx.index_select(0, rr)),
+                      v64, z64, "bf16 32768x128256 K=50 sample")
