@@ -117,6 +117,14 @@ OSM_API int softmax_topk(const float* x, float* vals, int32_t* idx, int64_t N, i
 OSM_API int softmax_topk_dt(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
                     int dtype, hipStream_t stream);
 
+/* softmax_topk_dt with an explicit kernel shape: kernel OSM_KERNEL_AUTO (what
+ * softmax_topk_dt uses; param ignored) or OSM_KERNEL_ROWS with param = lanes
+ * per row: 64, 128 or 256 (one, two or four wavefronts per row).  Results
+ * are identical across shapes except for binary32 rounding of vals.
+ * Errors: as softmax_topk_dt, plus OSM_EINVAL for another kernel or param. */
+OSM_API int softmax_topk_ex(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V,
+                            int K, int dtype, int kernel, int64_t param, hipStream_t stream);
+
 /* Kernel family and parameter softmax_fwd would use for this shape on the
  * current device.  Errors: OSM_EINVAL for bad sizes, dtype or null outputs. */
 OSM_API int osm_plan(int64_t N, int64_t V, int dtype, int mode, int* kernel, int64_t* param);

@@ -50,6 +50,8 @@ def lib() -> ctypes.CDLL:
     L.softmax_topk.restype = i32
     L.softmax_topk_dt.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
     L.softmax_topk_dt.restype = i32
+    L.softmax_topk_ex.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, i64, vp]
+    L.softmax_topk_ex.restype = i32
     L.osm_plan.argtypes = [i64, i64, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i64)]
     L.osm_plan.restype = i32
     L.osm_status_string.argtypes = [i32]
@@ -115,9 +117,11 @@ def softmax_fwd(x: torch.Tensor, y: torch.Tensor | None = None, mode="online",
 
 
 def softmax_topk(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,
-                 idx: torch.Tensor | None = None, stream=None):
+                 idx: torch.Tensor | None = None, stream=None, kernel: int = KERNEL_AUTO,
+                 param: int = 0):
     """(vals, idx) = fused softmax + top-k per row via ``softmax_topk``
-    (binary32 rows) or ``softmax_topk_dt`` (bfloat16 rows)."""
+    (binary32 rows), ``softmax_topk_dt`` (bfloat16 rows) or, with an explicit
+    kernel shape, ``softmax_topk_ex``."""
     N, V = _batch(x)
     if vals is None:
         vals = torch.empty((N, K), dtype=torch.float32, device=x.device)
@@ -127,7 +131,11 @@ def softmax_topk(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,
         if (t.dtype != dt or not t.is_contiguous() or t.numel() != N * K
                 or t.device != x.device):
             raise ValueError(f"{nm} must be a contiguous {dt} tensor of N*K elements on x's device")
-    if x.dtype == torch.float32:
+    if kernel != KERNEL_AUTO:
+        rc = lib().softmax_topk_ex(x.data_ptr(), vals.data_ptr(), idx.data_ptr(), N, V,
+                                   int(K), _DTYPES[x.dtype], int(kernel), int(param),
+                                   _stream(stream))
+    elif x.dtype == torch.float32:
         rc = lib().softmax_topk(x.data_ptr(), vals.data_ptr(), idx.data_ptr(), N, V, int(K),
                                 _stream(stream))
     else:

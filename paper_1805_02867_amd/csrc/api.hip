@@ -97,7 +97,7 @@ Plan choose(int64_t N, int64_t V, int dtype, int cus) {
         if (S >= 2) return {OSM_KERNEL_SPLIT, S};
     }
     if (nv <= 2048) return {OSM_KERNEL_ROWS, 256};
-    if (nv <= 8192) return {OSM_KERNEL_ROWS, 512};
+    if (nv <= 4096) return {OSM_KERNEL_ROWS, 512};
     return {OSM_KERNEL_ROWS, 1024};
 }
 
@@ -153,19 +153,29 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
     return hip_status(f);
 }
 
+// Top-k shape: one wavefront per row once the batch alone can give every
+// SIMD several wavefronts; otherwise a workgroup (four wavefronts) per row.
+int64_t topk_lanes(int64_t N, int cus) { return N >= 4 * (int64_t)cus ? 64 : 256; }
+
 int run_topk(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K, int dtype,
-             hipStream_t stream) {
+             int kernel, int64_t param, hipStream_t stream) {
     size_t bytes = 0;
     if (!check_shape(N, V, dtype, &bytes)) return OSM_EINVAL;
     if (K < 1 || K > OSM_TOPK_KMAX || (int64_t)K > V) return OSM_EINVAL;
+    if (kernel != OSM_KERNEL_AUTO &&
+        !(kernel == OSM_KERNEL_ROWS && (param == 64 || param == 128 || param == 256)))
+        return OSM_EINVAL;
     if (N == 0) return OSM_OK;
     if (!x || !vals || !idx) return OSM_EINVAL;
     if (!aligned(x, elem_size(dtype)) || !aligned(vals, 4) || !aligned(idx, 4)) return OSM_EINVAL;
     const size_t ob = (size_t)N * (size_t)K * 4;
     if (overlaps(x, bytes, vals, ob) || overlaps(x, bytes, idx, ob) || overlaps(vals, ob, idx, ob))
         return OSM_EINVAL;
-    if (!device_state(nullptr)) return OSM_EHIP;
-    return hip_status(osm::launch_topk_fused(x, vals, idx, N, V, K, dtype, true, stream));
+    DeviceState* ds = device_state(nullptr);
+    if (!ds) return OSM_EHIP;
+    const int64_t lanes = kernel == OSM_KERNEL_AUTO ? topk_lanes(N, ds->cus) : param;
+    return hip_status(
+        osm::launch_topk_fused(x, vals, idx, N, V, K, dtype, (int)(lanes / 64), stream));
 }
 
 }  // namespace
@@ -184,12 +194,17 @@ int softmax_fwd_ex(const void* x, void* y, int64_t N, int64_t V, int dtype, int 
 
 int softmax_topk(const float* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
                  hipStream_t stream) {
-    return run_topk(x, vals, idx, N, V, K, OSM_F32, stream);
+    return run_topk(x, vals, idx, N, V, K, OSM_F32, OSM_KERNEL_AUTO, 0, stream);
 }
 
 int softmax_topk_dt(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
                     int dtype, hipStream_t stream) {
-    return run_topk(x, vals, idx, N, V, K, dtype, stream);
+    return run_topk(x, vals, idx, N, V, K, dtype, OSM_KERNEL_AUTO, 0, stream);
+}
+
+int softmax_topk_ex(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
+                    int dtype, int kernel, int64_t param, hipStream_t stream) {
+    return run_topk(x, vals, idx, N, V, K, dtype, kernel, param, stream);
 }
 
 int osm_plan(int64_t N, int64_t V, int dtype, int mode, int* kernel, int64_t* param) {

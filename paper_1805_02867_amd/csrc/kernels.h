@@ -17,8 +17,9 @@ hipError_t launch_softmax_split(const void* x, void* y, void* scratch, int64_t N
                                 int dtype, int mode, int64_t S, int64_t chunk, bool vec,
                                 hipStream_t st);
 
-// Fused online softmax + top-k, one row per workgroup.
+// Fused online softmax + top-k; waves_per_row = 1 (four rows per workgroup)
+// or 4 (one row per workgroup).
 hipError_t launch_topk_fused(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V,
-                             int K, int dtype, bool vec, hipStream_t st);
+                             int K, int dtype, int waves_per_row, hipStream_t st);
 
 }  // namespace osm

@@ -134,10 +134,46 @@ __device__ __forceinline__ MD md_merge(MD a, MD b) {
 // every element enters as (x_j, 1), merged into the running pair.  One
 // rescale of the running d per vector, one exponential per element.
 template <int N>
-__device__ __forceinline__ MD md_fold(MD a, const float (&x)[N]) {
+__device__ __forceinline__ float vec_max(const float (&x)[N]) {
     float mx = x[0];
 #pragma unroll
     for (int i = 1; i < N; ++i) mx = fmaxf(mx, x[i]);
+    return mx;
+}
+
+// As md_fold, with the vector's maximum already at hand.
+template <int N>
+__device__ __forceinline__ MD md_fold_mx(MD a, const float (&x)[N], float mx) {
+    float S = fmaxf(a.s, mx * kLog2e);
+    float acc = a.d * exp2_hw(a.s - S);
+#pragma unroll
+    for (int i = 0; i < N; ++i) acc += exp2_hw(__builtin_fmaf(x[i], kLog2e, -S));
+    return MD{S, acc};
+}
+
+// Lazy variant for the one-pass loops: the reference s moves only when a
+// vector's maximum exceeds it by more than kLazy (in log2 units), so most
+// vectors skip the rescale and its exponential.  d = sum 2^{x log2e - s}
+// holds for any s; with s >= max * log2e - kLazy every term stays <= 2^kLazy
+// (d <= 2^kLazy * V: no overflow for any V < 2^31).
+constexpr float kLazy = 8.0f;
+
+template <int N>
+__device__ __forceinline__ MD md_fold_lazy(MD a, const float (&x)[N], float mx) {
+    const float t = mx * kLog2e;
+    if (t > a.s + kLazy) {  // divergent, rarely taken after a lane's first vectors
+        a.d *= exp2_hw(a.s - t);
+        a.s = t;
+    }
+    float acc = a.d;
+#pragma unroll
+    for (int i = 0; i < N; ++i) acc += exp2_hw(__builtin_fmaf(x[i], kLog2e, -a.s));
+    return MD{a.s, acc};
+}
+
+template <int N>
+__device__ __forceinline__ MD md_fold(MD a, const float (&x)[N]) {
+    float mx = vec_max(x);
     float S = fmaxf(a.s, mx * kLog2e);
     float acc = a.d * exp2_hw(a.s - S);
 #pragma unroll
@@ -151,60 +187,91 @@ __device__ __forceinline__ MD md_fold1(MD a, float x) {
 }
 
 // ------------------------------------------------------- lane-group exchange
-// Value of lane (lane ^ MASK); MASK < 64.  Quad permutations for 1 and 2,
-// the LDS crossbar swizzle (no memory traffic) for 4..16, and a bpermute for
-// 32.  All lanes taking part must be active.
-template <int MASK>
-__device__ __forceinline__ float xor_lane(float v) {
-    int i = __float_as_int(v);
-    int r;
-    if constexpr (MASK == 1) {
-        r = __builtin_amdgcn_update_dpp(0, i, 0xB1, 0xF, 0xF, false);  // [1,0,3,2]
-    } else if constexpr (MASK == 2) {
-        r = __builtin_amdgcn_update_dpp(0, i, 0x4E, 0xF, 0xF, false);  // [2,3,0,1]
-    } else if constexpr (MASK == 4 || MASK == 8 || MASK == 16) {
-        r = __builtin_amdgcn_ds_swizzle(i, (MASK << 10) | 0x1F);
-    } else {
-        static_assert(MASK == 32, "xor_lane: mask must be a power of two below 64");
-        int src = ((int)__lane_id() ^ 32) << 2;
-        r = __builtin_amdgcn_ds_bpermute(src, i);
-    }
-    return __int_as_float(r);
-}
-
-template <int MASK>
-__device__ __forceinline__ uint32_t xor_lane_u(uint32_t v) {
-    return (uint32_t)__float_as_int(xor_lane<MASK>(__int_as_float((int)v)));
-}
-
 // Butterfly reductions over aligned groups of G lanes (G a power of two,
-// 1..64).  Every lane of a group ends with the same value bit for bit: each
-// step combines a value with its partner's through a symmetric operator.
-template <int G, int MASK = 1>
-__device__ __forceinline__ MD group_merge(MD a) {
-    if constexpr (MASK < G) {
-        MD b{xor_lane<MASK>(a.s), xor_lane<MASK>(a.d)};
-        return group_merge<G, MASK * 2>(md_merge(a, b));
+// 1..64) entirely in VALU cross-lane operations, no LDS round trips:
+//   step 0: DPP quad_perm [1,0,3,2]      (pairs lanes i, i^1)
+//   step 1: DPP quad_perm [2,3,0,1]      (pairs lanes i, i^2)
+//   step 2: DPP row_half_mirror          (pairs i, 7-i within 8 lanes)
+//   step 3: DPP row_mirror               (pairs i, 15-i within 16 lanes)
+//   step 4: v_permlane16_swap            (pairs 16-lane rows 2r, 2r+1)
+//   step 5: v_permlane32_swap            (pairs the two 32-lane halves)
+// After steps 0..k-1 every lane of an aligned group of 2^k lanes holds the
+// same bits: at steps 0-1 values are paired with their xor partner; at steps
+// 2-3 all lanes of each half of the group already agree, so a mirror pairs
+// the halves; at steps 4-5 each swap hands both lanes of a pair the same two
+// operands in the same order.  The operator must be commutative bit for bit
+// (max, +, and the merge of Eq. 4 as written below are).  All lanes of a
+// group must be active.
+template <int STEP>
+__device__ __forceinline__ void bfly_operands(uint32_t v, uint32_t& a, uint32_t& b) {
+    if constexpr (STEP == 0) {
+        a = v;
+        b = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+    } else if constexpr (STEP == 1) {
+        a = v;
+        b = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+    } else if constexpr (STEP == 2) {
+        a = v;
+        b = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false);
+    } else if constexpr (STEP == 3) {
+        a = v;
+        b = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false);
+    } else if constexpr (STEP == 4) {
+        auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        a = p[0];
+        b = p[1];
     } else {
-        return a;
+        static_assert(STEP == 5, "a 64-lane butterfly has six steps");
+        auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        a = p[0];
+        b = p[1];
     }
 }
 
-template <int G, int MASK = 1>
-__device__ __forceinline__ float group_max(float a) {
-    if constexpr (MASK < G) {
-        return group_max<G, MASK * 2>(fmaxf(a, xor_lane<MASK>(a)));
+template <int STEP>
+__device__ __forceinline__ void bfly_operands(float v, float& a, float& b) {
+    uint32_t ua, ub;
+    bfly_operands<STEP>(__float_as_uint(v), ua, ub);
+    a = __uint_as_float(ua);
+    b = __uint_as_float(ub);
+}
+
+template <int STEP>
+__device__ __forceinline__ void bfly_operands(MD v, MD& a, MD& b) {
+    bfly_operands<STEP>(v.s, a.s, b.s);
+    bfly_operands<STEP>(v.d, a.d, b.d);
+}
+
+template <int G, int STEP = 0>
+__device__ __forceinline__ MD group_merge(MD v) {
+    if constexpr ((1 << STEP) < G) {
+        MD a, b;
+        bfly_operands<STEP>(v, a, b);
+        return group_merge<G, STEP + 1>(md_merge(a, b));
     } else {
-        return a;
+        return v;
     }
 }
 
-template <int G, int MASK = 1>
-__device__ __forceinline__ float group_sum(float a) {
-    if constexpr (MASK < G) {
-        return group_sum<G, MASK * 2>(a + xor_lane<MASK>(a));
+template <int G, int STEP = 0>
+__device__ __forceinline__ float group_max(float v) {
+    if constexpr ((1 << STEP) < G) {
+        float a, b;
+        bfly_operands<STEP>(v, a, b);
+        return group_max<G, STEP + 1>(fmaxf(a, b));
     } else {
-        return a;
+        return v;
+    }
+}
+
+template <int G, int STEP = 0>
+__device__ __forceinline__ float group_sum(float v) {
+    if constexpr ((1 << STEP) < G) {
+        float a, b;
+        bfly_operands<STEP>(v, a, b);
+        return group_sum<G, STEP + 1>(a + b);
+    } else {
+        return v;
     }
 }
 

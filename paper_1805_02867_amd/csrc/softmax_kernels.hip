@@ -25,9 +25,25 @@
 #include "md.hpp"
 #include "kernels.h"
 
+// Load cache policy per pass: a pass whose loads are the last use of the
+// data (the output pass) reads with non-temporal hints; earlier passes use
+// ordinary loads so their lines can serve the re-read.
+#ifndef OSM_NT_FIRST
+#define OSM_NT_FIRST 0
+#endif
+#ifndef OSM_NT_LAST
+#define OSM_NT_LAST 1
+#endif
+
 namespace osm {
 
 enum { NAIVE = 0, SAFE = 1, ONLINE = 2 };
+
+template <typename T, bool NT>
+__device__ __forceinline__ Vec<T> vload(const T* p) {
+    if constexpr (NT) return Vec<T>::load_nt(p);
+    else return Vec<T>::load(p);
+}
 
 // The part of a row a team works on, split into scalar head, aligned vector
 // body and scalar tail.
@@ -61,7 +77,7 @@ struct Range {
 // ------------------------------------------------------------ per-lane folds
 // Online pass 1 over the lane's share of a range: U independent pairs (one
 // per unrolled load) keep U loads in flight and shorten the dependency chain.
-template <typename T, int TEAM, int U>
+template <typename T, int TEAM, int U, bool NT = OSM_NT_FIRST>
 __device__ __forceinline__ MD lane_md(const Range<T>& r, int t) {
     constexpr int E = Vec<T>::N;
     MD st[U];
@@ -72,11 +88,14 @@ __device__ __forceinline__ MD lane_md(const Range<T>& r, int t) {
     for (; v + (int64_t)(U - 1) * TEAM < r.nvec; v += (int64_t)U * TEAM) {
         Vec<T> buf[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) buf[u] = Vec<T>::load(vb + (v + (int64_t)u * TEAM) * E);
+        for (int u = 0; u < U; ++u) buf[u] = vload<T, NT>(vb + (v + (int64_t)u * TEAM) * E);
 #pragma unroll
-        for (int u = 0; u < U; ++u) st[u] = md_fold(st[u], buf[u].v);
+        for (int u = 0; u < U; ++u) st[u] = md_fold_lazy(st[u], buf[u].v, vec_max(buf[u].v));
     }
-    for (; v < r.nvec; v += TEAM) st[0] = md_fold(st[0], Vec<T>::load(vb + v * E).v);
+    for (; v < r.nvec; v += TEAM) {
+        Vec<T> b = vload<T, NT>(vb + v * E);
+        st[0] = md_fold_lazy(st[0], b.v, vec_max(b.v));
+    }
     for (int64_t i = t; i < r.head; i += TEAM) st[0] = md_fold1(st[0], load1(r.xb + i));
     for (int64_t i = r.tail0 + t; i < r.n; i += TEAM) st[0] = md_fold1(st[0], load1(r.xb + i));
     MD acc = st[0];
@@ -93,7 +112,7 @@ __device__ __forceinline__ float vmax(float m, const float (&x)[N]) {
 }
 
 // Safe pass 1: the maximum of the lane's share.
-template <typename T, int TEAM, int U>
+template <typename T, int TEAM, int U, bool NT = OSM_NT_FIRST>
 __device__ __forceinline__ float lane_max(const Range<T>& r, int t) {
     constexpr int E = Vec<T>::N;
     float m[U];
@@ -104,11 +123,11 @@ __device__ __forceinline__ float lane_max(const Range<T>& r, int t) {
     for (; v + (int64_t)(U - 1) * TEAM < r.nvec; v += (int64_t)U * TEAM) {
         Vec<T> buf[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) buf[u] = Vec<T>::load(vb + (v + (int64_t)u * TEAM) * E);
+        for (int u = 0; u < U; ++u) buf[u] = vload<T, NT>(vb + (v + (int64_t)u * TEAM) * E);
 #pragma unroll
         for (int u = 0; u < U; ++u) m[u] = vmax(m[u], buf[u].v);
     }
-    for (; v < r.nvec; v += TEAM) m[0] = vmax(m[0], Vec<T>::load(vb + v * E).v);
+    for (; v < r.nvec; v += TEAM) m[0] = vmax(m[0], vload<T, NT>(vb + v * E).v);
     for (int64_t i = t; i < r.head; i += TEAM) m[0] = fmaxf(m[0], load1(r.xb + i));
     for (int64_t i = r.tail0 + t; i < r.n; i += TEAM) m[0] = fmaxf(m[0], load1(r.xb + i));
     float acc = m[0];
@@ -126,7 +145,7 @@ __device__ __forceinline__ float vsum_exp(float a, const float (&x)[N], float S)
 
 // Sum of 2^{x log2e - S} over the lane's share (naive pass 1 with S = 0,
 // safe pass 2 with S = max * log2e).
-template <typename T, int TEAM, int U>
+template <typename T, int TEAM, int U, bool NT = OSM_NT_FIRST>
 __device__ __forceinline__ float lane_sum(const Range<T>& r, int t, float S) {
     constexpr int E = Vec<T>::N;
     float a[U];
@@ -137,11 +156,11 @@ __device__ __forceinline__ float lane_sum(const Range<T>& r, int t, float S) {
     for (; v + (int64_t)(U - 1) * TEAM < r.nvec; v += (int64_t)U * TEAM) {
         Vec<T> buf[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) buf[u] = Vec<T>::load(vb + (v + (int64_t)u * TEAM) * E);
+        for (int u = 0; u < U; ++u) buf[u] = vload<T, NT>(vb + (v + (int64_t)u * TEAM) * E);
 #pragma unroll
         for (int u = 0; u < U; ++u) a[u] = vsum_exp(a[u], buf[u].v, S);
     }
-    for (; v < r.nvec; v += TEAM) a[0] = vsum_exp(a[0], Vec<T>::load(vb + v * E).v, S);
+    for (; v < r.nvec; v += TEAM) a[0] = vsum_exp(a[0], vload<T, NT>(vb + v * E).v, S);
     for (int64_t i = t; i < r.head; i += TEAM)
         a[0] += exp2_hw(__builtin_fmaf(load1(r.xb + i), kLog2e, -S));
     for (int64_t i = r.tail0 + t; i < r.n; i += TEAM)
@@ -154,7 +173,7 @@ __device__ __forceinline__ float lane_sum(const Range<T>& r, int t, float S) {
 
 // Output pass: y = 2^{x log2e - S} * (1/d), stored with non-temporal hints so
 // that the written rows do not evict input rows still waiting for this pass.
-template <typename T, int TEAM, int U>
+template <typename T, int TEAM, int U, bool NT = OSM_NT_LAST>
 __device__ __forceinline__ void lane_out(const Range<T>& r, int t, float S, float rd) {
     constexpr int E = Vec<T>::N;
     const T* vb = r.xb + r.head;
@@ -163,7 +182,7 @@ __device__ __forceinline__ void lane_out(const Range<T>& r, int t, float S, floa
     for (; v + (int64_t)(U - 1) * TEAM < r.nvec; v += (int64_t)U * TEAM) {
         Vec<T> buf[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) buf[u] = Vec<T>::load(vb + (v + (int64_t)u * TEAM) * E);
+        for (int u = 0; u < U; ++u) buf[u] = vload<T, NT>(vb + (v + (int64_t)u * TEAM) * E);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
 #pragma unroll
@@ -173,7 +192,7 @@ __device__ __forceinline__ void lane_out(const Range<T>& r, int t, float S, floa
         }
     }
     for (; v < r.nvec; v += TEAM) {
-        Vec<T> b = Vec<T>::load(vb + v * E);
+        Vec<T> b = vload<T, NT>(vb + v * E);
 #pragma unroll
         for (int i = 0; i < E; ++i) b.v[i] = exp2_hw(__builtin_fmaf(b.v[i], kLog2e, -S)) * rd;
         b.store_nt(yb + v * E);

@@ -11,35 +11,51 @@
 //        (monotone image of x) << 32 | ~index,
 //    so a larger key means a larger x, or an equal x at a lower index: the
 //    order Alg. 4's strictly-less insertion produces.  -0.0 is keyed as +0.0.
-//  * Filter.  Each wavefront keeps its own top-K list (keys in LDS) and the
-//    threshold tau = its K-th key.  Those K elements belong to the row, so
-//    the row's K-th key is >= tau, and an element with key <= tau can never
-//    enter the row's top-K.  A cheap test on each lane's 16-byte vector maximum
-//    (already computed for the online pair) skips whole vectors.
+//  * Threshold.  Each wavefront keeps its own top-K list (keys in LDS); its
+//    K-th key is a key of K elements of the row, so the row's K-th key is at
+//    least as large, and no element with a key <= that threshold can enter
+//    the row's top-K.  When several wavefronts share a row they publish their
+//    thresholds in LDS and each filters with the largest one (tau).
+//  * Bootstrap.  Before the first selection, tau comes from the first step:
+//    the K-th largest distinct value among the lanes' maxima is the value of
+//    K distinct elements, so every top-K element is at least as large.
+//  * Filter.  Per 16-byte vector, the maximum (needed for the online pair
+//    anyway) is compared with tau's value: most vectors are skipped with one
+//    compare.  Otherwise each element is compared with tau's value, and only
+//    an element at or above it gets its key built and the exact key test
+//    (which settles ties by index).
 //  * Queue.  Elements that pass are appended to the wavefront's LDS queue
-//    (ballot + mbcnt compaction).
+//    right after its list (ballot + mbcnt compaction).
 //  * Select.  When the queue fills up, or holds enough entries to be worth
 //    raising tau, the wavefront selects the K largest keys of list + queue:
-//    K rounds of "largest key below the last one taken", each a scan of 5
-//    entries per lane and a 6-step butterfly maximum.
-//  * Merge.  At the end of the row, the pairs of the wavefronts are merged
-//    (Eq. 4) and wavefront 0 selects the K largest keys of all the lists.
-//    Outputs are v_i = 2^{x_i log2e - s} / d and z_i = index, in key order.
+//    K rounds of "largest key below the last one taken", each a scan of the
+//    occupied slots (one per lane per 64) and a 6-step butterfly maximum.
+//    Lane k ends holding the k-th key, so the list stays sorted.
+//  * Output.  The normalizer pairs are merged (Eq. 4) and the sorted list
+//    gives v_i = 2^{x_i log2e - s} / d and z_i = index, in key order.  With
+//    several wavefronts per row, wavefront 0 first selects the K largest keys
+//    of their lists.
+//
+// Three shapes: one, two or four wavefronts per row (four, two or one rows
+// per 256-thread workgroup).  Fewer wavefronts per row keep a row's filter
+// state in fewer hands (one wavefront needs no barrier at all); more give
+// each SIMD more wavefronts to hide the latency of the selection chains, and
+// fill the chip when the batch is small.  Each step issues all of a lane's loads
+// before processing any, so a wavefront keeps U KiB in flight; loads carry
+// non-temporal hints since every element is read exactly once.
 #include "md.hpp"
 #include "kernels.h"
 
 namespace osm {
 
 constexpr int TK_BLOCK = 256;
-constexpr int TK_W = TK_BLOCK / 64;
-constexpr int TK_KMAX = 64;          // largest supported K (one list slot per lane)
-constexpr int TK_QCAP = 256;         // queue entries per wavefront
-constexpr int TK_REGION = TK_KMAX + TK_QCAP;
+constexpr int TK_KMAX = 64;            // largest supported K (one list slot per lane)
+constexpr int TK_REGION = 320;         // list + queue slots per wavefront
 constexpr int TK_PER_LANE = TK_REGION / 64;
-constexpr int TK_FLUSH_AT = 128;     // select early once the queue holds this many
-constexpr int TK_U = 2;              // 16-byte vectors per lane in flight
+constexpr int TK_FLUSH_AT = 32;        // select early once the queue holds this many
 
 static_assert(TK_REGION % 64 == 0, "region must split evenly over 64 lanes");
+static_assert(TK_REGION - TK_KMAX >= 64, "the queue must take a full wavefront");
 
 __device__ __forceinline__ uint64_t make_key(float x, uint32_t idx) {
     uint32_t u = __float_as_uint(x);
@@ -56,31 +72,41 @@ __device__ __forceinline__ float key_value(uint64_t k) {
 
 __device__ __forceinline__ int32_t key_index(uint64_t k) { return (int32_t)(~(uint32_t)k); }
 
-// Largest key over the wavefront; every lane gets the same value.
-__device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
-    uint32_t hi = (uint32_t)(k >> 32), lo = (uint32_t)k;
-#define OSM_KEY_STEP(M)                                                  \
-    {                                                                    \
-        uint32_t oh = xor_lane_u<M>(hi), ol = xor_lane_u<M>(lo);         \
-        bool take = (oh > hi) || (oh == hi && ol > lo);                  \
-        hi = take ? oh : hi;                                             \
-        lo = take ? ol : lo;                                             \
-    }
-    OSM_KEY_STEP(1)
-    OSM_KEY_STEP(2)
-    OSM_KEY_STEP(4)
-    OSM_KEY_STEP(8)
-    OSM_KEY_STEP(16)
-    OSM_KEY_STEP(32)
-#undef OSM_KEY_STEP
-    return ((uint64_t)hi << 32) | lo;
+// Largest key over the wavefront (six butterfly steps of md.hpp); every lane
+// gets the same value.
+template <int STEP>
+__device__ __forceinline__ uint64_t key_bfly(uint64_t k) {
+    uint32_t ah, bh, al, bl;
+    bfly_operands<STEP>((uint32_t)(k >> 32), ah, bh);
+    bfly_operands<STEP>((uint32_t)k, al, bl);
+    const uint64_t a = ((uint64_t)ah << 32) | al, b = ((uint64_t)bh << 32) | bl;
+    return a > b ? a : b;
 }
 
-// Selection of the K largest keys among n_per_lane * 64 slots (0 = empty).
-// Lane k returns the k-th largest key (0 past the available count); the
-// number found is returned in *found.
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
+    k = key_bfly<0>(k);
+    k = key_bfly<1>(k);
+    k = key_bfly<2>(k);
+    k = key_bfly<3>(k);
+    k = key_bfly<4>(k);
+    k = key_bfly<5>(k);
+    return k;
+}
+
+// The same 64-bit value on every lane, taken from lane `src` (uniform).
+__device__ __forceinline__ uint64_t read_lane_key(uint64_t k, int src) {
+    // readlane returns int: go through uint32_t so that the low word is
+    // zero-extended, not sign-extended
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)k, src);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(k >> 32), src);
+    return ((uint64_t)hi << 32) | (uint64_t)lo;
+}
+
+// Selection of the K largest keys among the first `rows` of PER_LANE slots
+// per lane (0 = empty).  Lane k returns the k-th largest key (0 past the
+// available count); the number found is returned in *found.
 template <int PER_LANE>
-__device__ __forceinline__ uint64_t select_topk(const uint64_t (&e)[PER_LANE], int K,
+__device__ __forceinline__ uint64_t select_topk(const uint64_t (&e)[PER_LANE], int rows, int K,
                                                 int* found) {
     const int lane = __lane_id();
     uint64_t last = ~0ull, mine = 0;
@@ -89,8 +115,10 @@ __device__ __forceinline__ uint64_t select_topk(const uint64_t (&e)[PER_LANE], i
         uint64_t best = 0;
 #pragma unroll
         for (int j = 0; j < PER_LANE; ++j) {
-            uint64_t c = e[j];
-            best = (c < last && c > best) ? c : best;
+            if (j < rows) {
+                uint64_t c = e[j];
+                best = (c < last && c > best) ? c : best;
+            }
         }
         best = wave_max_key(best);
         if (best == 0) break;
@@ -101,180 +129,302 @@ __device__ __forceinline__ uint64_t select_topk(const uint64_t (&e)[PER_LANE], i
     return mine;
 }
 
+template <int W>  // wavefronts sharing a row
 struct TopkWave {
-    uint64_t* region;  // [0, KMAX): sorted list; [KMAX, REGION): queue
+    uint64_t* region;      // [0, K): sorted list; [K, K + qcount): queue
+    uint64_t* published;   // thresholds of the wavefronts of the row (W > 1)
+    int wave;              // index of this wavefront within its row
+    int K;
     int qcount;
     uint64_t tau;
     float tau_v;
+    uint64_t mine;         // lane k: k-th key of the list (after a selection)
 
-    // list + queue -> new list; resets the queue; raises tau.
-    __device__ __forceinline__ void flush(int K) {
-        const int lane = __lane_id();
-        wave_sync();
-        uint64_t e[TK_PER_LANE];
-#pragma unroll
-        for (int j = 0; j < TK_PER_LANE; ++j) e[j] = region[lane + 64 * j];
-        int found;
-        uint64_t mine = select_topk<TK_PER_LANE>(e, K, &found);
-        wave_sync();
-        region[lane] = mine;
-#pragma unroll
-        for (int j = 1; j < TK_PER_LANE; ++j) region[lane + 64 * j] = 0;
-        wave_sync();
-        qcount = 0;
-        if (found == K) {
-            // readlane returns int: go through uint32_t so that the low word
-            // is zero-extended, not sign-extended
-            const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)mine, K - 1);
-            const uint32_t hi =
-                (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(mine >> 32), K - 1);
-            tau = ((uint64_t)hi << 32) | (uint64_t)lo;
-            tau_v = key_value(tau);
+    __device__ __forceinline__ void raise_tau(uint64_t t) {
+        if (t > tau) {
+            tau = t;
+            tau_v = key_value(t);
         }
     }
 
-    // Offer one element per lane (ok = lane holds a real element).
-    __device__ __forceinline__ void offer(float x, uint32_t idx, bool ok, int K) {
-        uint64_t key = make_key(x, idx);
-        bool p = ok && key > tau;
+    // list + queue -> new list; resets the queue; raises (and publishes) tau.
+    __device__ __forceinline__ void flush() {
+        const int lane = __lane_id();
+        const int used = K + qcount;
+        const int rows = (used + 63) >> 6;
+        wave_sync();
+        uint64_t e[TK_PER_LANE];
+#pragma unroll
+        for (int j = 0; j < TK_PER_LANE; ++j)
+            e[j] = (j < rows && lane + 64 * j < used) ? region[lane + 64 * j] : 0ull;
+        int found;
+        mine = select_topk<TK_PER_LANE>(e, rows, K, &found);
+        wave_sync();
+        if (lane < K) region[lane] = mine;
+        wave_sync();
+        qcount = 0;
+        if (found == K) {
+            raise_tau(read_lane_key(mine, K - 1));
+            if constexpr (W > 1) {
+                // other wavefronts read this without a barrier: a single-copy
+                // atomic 64-bit store keeps them from seeing a torn key
+                if (lane == 0)
+                    __hip_atomic_store(&published[wave], tau, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+        }
+    }
+
+    // Take the largest threshold any wavefront of the row has published.
+    __device__ __forceinline__ void pull() {
+        if constexpr (W > 1) {
+            uint64_t t = 0;
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+                uint64_t o = __hip_atomic_load(&published[w], __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_WORKGROUP);
+                t = o > t ? o : t;
+            }
+            raise_tau(t);
+        }
+    }
+
+    // Append the lanes' keys where p holds.
+    __device__ __forceinline__ void append(bool p, uint64_t key) {
         uint64_t mask = __builtin_amdgcn_ballot_w64(p);
         if (mask == 0) return;
         int cnt = __builtin_popcountll(mask);
-        if (qcount + cnt > TK_QCAP) {
-            flush(K);
-            p = ok && key > tau;
+        if (K + qcount + cnt > TK_REGION) {
+            flush();
+            p = p && key > tau;
             mask = __builtin_amdgcn_ballot_w64(p);
             cnt = __builtin_popcountll(mask);
         }
         uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
                                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-        if (p) region[TK_KMAX + qcount + below] = key;
+        if (p) region[K + qcount + below] = key;
         qcount += cnt;
+    }
+
+    // Offer E consecutive elements per lane (indices idx0 .. idx0 + E - 1).
+    template <int E>
+    __device__ __forceinline__ void offer(const float (&x)[E], uint32_t idx0, bool ok) {
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+            bool p = ok && x[i] >= tau_v;
+            if (__builtin_amdgcn_ballot_w64(p) != 0) {
+                uint64_t key = make_key(x[i], idx0 + (uint32_t)i);
+                append(p && key > tau, key);
+            }
+        }
     }
 };
 
-template <typename T, bool VEC>
-__global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
-                                                      float* __restrict__ vals,
-                                                      int32_t* __restrict__ idx, int64_t V,
-                                                      int K) {
-    constexpr int E = Vec<T>::N;
-    __shared__ uint64_t region[TK_W][TK_REGION];
-    __shared__ MD wmd[TK_W];
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t row = blockIdx.x;
-    const T* xr = x + row * V;
-
-    for (int i = tid; i < TK_W * TK_REGION; i += TK_BLOCK) (&region[0][0])[i] = 0;
-    __syncthreads();
-
-    TopkWave tw{region[wave], 0, 0ull, -__builtin_inff()};
-
-    // split of the row into scalar head, 16-byte vectors, scalar tail
-    int64_t head, nvec;
-    if (VEC) {
-        int64_t mis = (int64_t)(((uintptr_t)xr) & 15);
-        head = ((16 - mis) & 15) / (int64_t)sizeof(T);
-        if (head > V) head = V;
-        nvec = (V - head) / E;
+// Raw 16-byte vector and its widening to binary32.
+template <typename T>
+__device__ __forceinline__ void widen(u32x4 q, float (&x)[Vec<T>::N]) {
+    if constexpr (Vec<T>::N == 4) {
+        x[0] = __uint_as_float(q.x);
+        x[1] = __uint_as_float(q.y);
+        x[2] = __uint_as_float(q.z);
+        x[3] = __uint_as_float(q.w);
     } else {
-        head = V;
-        nvec = 0;
-    }
-    const int64_t tail0 = head + nvec * E;
-    const T* vb = xr + head;
-
-    MD st[TK_U];
-#pragma unroll
-    for (int u = 0; u < TK_U; ++u) st[u] = md_empty();
-
-    // scalar head and tail: wave-uniform loops, one element per lane
-    for (int64_t b0 = 0; b0 < head; b0 += TK_BLOCK) {
-        int64_t i = b0 + tid;
-        bool ok = i < head;
-        float v = ok ? load1(xr + i) : -__builtin_inff();
-        if (ok) st[0] = md_fold1(st[0], v);
-        tw.offer(v, (uint32_t)i, ok, K);
-    }
-    for (int64_t b0 = tail0; b0 < V; b0 += TK_BLOCK) {
-        int64_t i = b0 + tid;
-        bool ok = i < V;
-        float v = ok ? load1(xr + i) : -__builtin_inff();
-        if (ok) st[0] = md_fold1(st[0], v);
-        tw.offer(v, (uint32_t)i, ok, K);
-    }
-
-    // vector body: every lane runs the same number of iterations so that the
-    // wavefront-wide queue operations see all 64 lanes
-    for (int64_t b0 = 0; b0 < nvec; b0 += (int64_t)TK_BLOCK * TK_U) {
-        Vec<T> buf[TK_U];
-        bool ok[TK_U];
-#pragma unroll
-        for (int u = 0; u < TK_U; ++u) {
-            int64_t vi = b0 + (int64_t)u * TK_BLOCK + tid;
-            ok[u] = vi < nvec;
-            buf[u] = ok[u] ? Vec<T>::load(vb + vi * E) : Vec<T>::fill(-__builtin_inff());
-        }
-#pragma unroll
-        for (int u = 0; u < TK_U; ++u) {
-            float mx = buf[u].v[0];
-#pragma unroll
-            for (int i = 1; i < E; ++i) mx = fmaxf(mx, buf[u].v[i]);
-            st[u] = md_fold(st[u], buf[u].v);
-            if (__builtin_amdgcn_ballot_w64(ok[u] && mx >= tw.tau_v) != 0) {
-                const int64_t e0 = head + (b0 + (int64_t)u * TK_BLOCK + tid) * E;
-#pragma unroll
-                for (int i = 0; i < E; ++i) tw.offer(buf[u].v[i], (uint32_t)(e0 + i), ok[u], K);
-            }
-        }
-        if (tw.qcount >= TK_FLUSH_AT) tw.flush(K);
-    }
-    tw.flush(K);
-
-    // merge of the normalizer pairs: wavefront butterflies, then fixed order
-    MD md = st[0];
-#pragma unroll
-    for (int u = 1; u < TK_U; ++u) md = md_merge(md, st[u]);
-    md = group_merge<64>(md);
-    if (lane == 0) wmd[wave] = md;
-    __syncthreads();
-    if (wave == 0) {
-        MD r = wmd[0];
-#pragma unroll
-        for (int w = 1; w < TK_W; ++w) r = md_merge(r, wmd[w]);
-        const float S = r.s, rd = 1.0f / r.d;
-        uint64_t e[TK_W];
-#pragma unroll
-        for (int w = 0; w < TK_W; ++w) e[w] = region[w][lane];
-        int found;
-        uint64_t mine = select_topk<TK_W>(e, K, &found);
-        if (lane < K) {
-            float xv = key_value(mine);
-            vals[row * K + lane] = exp2_hw(__builtin_fmaf(xv, kLog2e, -S)) * rd;
-            idx[row * K + lane] = key_index(mine);
-        }
+        x[0] = bf16_lo(q.x); x[1] = bf16_hi(q.x);
+        x[2] = bf16_lo(q.y); x[3] = bf16_hi(q.y);
+        x[4] = bf16_lo(q.z); x[5] = bf16_hi(q.z);
+        x[6] = bf16_lo(q.w); x[7] = bf16_hi(q.w);
     }
 }
 
+// W wavefronts per row; TK_BLOCK / (64 W) rows per workgroup; U 16-byte
+// vectors per lane per step, all loaded before any is processed.
+template <typename T, int W, int U>
+__global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
+                                                      float* __restrict__ vals,
+                                                      int32_t* __restrict__ idx, int64_t N,
+                                                      int64_t V, int K) {
+    constexpr int E = Vec<T>::N;
+    constexpr int WB = TK_BLOCK / 64;       // wavefronts per workgroup
+    constexpr int RB = WB / W;              // rows per workgroup
+    constexpr int TR = 64 * W;              // threads per row
+    constexpr int64_t STEP = (int64_t)TR * U;
+    __shared__ uint64_t region[WB][TK_REGION];
+    __shared__ uint64_t published[WB];
+    __shared__ MD wmd[WB];
+
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int rw = wv % W;                  // wavefront within the row
+    const int tr = tid % TR;                // thread within the row
+    const int64_t row = (int64_t)blockIdx.x * RB + wv / W;
+    const bool live = row < N;              // uniform per wavefront (and per row)
+
+    if (lane < K) region[wv][lane] = 0;     // empty list
+    if (lane == 0) published[wv] = 0;
+    if constexpr (W > 1) __syncthreads();
+    if (!live) return;                      // whole rows leave together
+
+    const T* xr = x + row * V;
+    TopkWave<W> tw{region[wv], published + (wv / W) * W, rw, K, 0, 0ull, -__builtin_inff(),
+                   0ull};
+
+    // split of the row into scalar head, 16-byte vectors, scalar tail
+    int64_t head = ((16 - (int64_t)(((uintptr_t)xr) & 15)) & 15) / (int64_t)sizeof(T);
+    if (head > V) head = V;
+    const int64_t nvec = (V - head) / E;
+    const int64_t tail0 = head + nvec * E;
+    const u32x4* vb = reinterpret_cast<const u32x4*>(xr + head);
+
+    MD st[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) st[u] = md_empty();
+
+    // scalar head and tail: wave-uniform loops, one element per lane
+    for (int64_t b0 = 0; b0 < head; b0 += TR) {
+        int64_t i = b0 + tr;
+        bool ok = i < head;
+        float v[1] = {ok ? load1(xr + i) : -__builtin_inff()};
+        if (ok) st[0] = md_fold1(st[0], v[0]);
+        tw.template offer<1>(v, (uint32_t)i, ok);
+    }
+    for (int64_t b0 = tail0; b0 < V; b0 += TR) {
+        int64_t i = b0 + tr;
+        bool ok = i < V;
+        float v[1] = {ok ? load1(xr + i) : -__builtin_inff()};
+        if (ok) st[0] = md_fold1(st[0], v[0]);
+        tw.template offer<1>(v, (uint32_t)i, ok);
+    }
+
+    // vector body: every lane runs the same number of steps so that the
+    // wavefront-wide queue operations see all 64 lanes
+    const u32x4 ninf = (E == 4) ? u32x4{0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u}
+                                : u32x4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
+    // Loads are unconditional (an index past the row is clamped to the last
+    // vector and its data masked afterwards): a load under a branch would
+    // stop the compiler from counting outstanding loads and make it wait for
+    // all of them.
+    const int64_t vlast = nvec > 0 ? nvec - 1 : 0;
+    auto load = [&](u32x4 (&buf)[U], bool (&ok)[U], int64_t b0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t vi = b0 + (int64_t)u * TR + tr;
+            ok[u] = vi < nvec;
+            buf[u] = __builtin_nontemporal_load(vb + (vi < nvec ? vi : vlast));
+        }
+    };
+    auto widen_ok = [&](u32x4 q, bool ok, float (&xv)[E]) { widen<T>(ok ? q : ninf, xv); };
+
+    u32x4 buf[U];
+    bool ok[U];
+    for (int64_t b0 = 0; b0 < nvec; b0 += STEP) {
+        load(buf, ok, b0);
+        if (b0 == 0) {
+            // Bootstrap: the K-th largest distinct value among the lanes'
+            // first-step maxima bounds the row's K-th value from below; keys
+            // >= (that value, any index) are kept, i.e. keys > (value key with
+            // index word 0) - 1.
+            float lm = -__builtin_inff();
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                float xv[E];
+                widen_ok(buf[u], ok[u], xv);
+                lm = fmaxf(lm, vec_max(xv));
+            }
+            float last = __builtin_inff();
+            int k = 0;
+            for (; k < K; ++k) {
+                float c = (lm < last) ? lm : -__builtin_inff();
+                c = group_max<64>(c);
+                if (!(c > -__builtin_inff())) break;
+                last = c;
+            }
+            if (k == K) tw.raise_tau((make_key(last, 0u) & 0xFFFFFFFF00000000ull) - 1);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            float xv[E];
+            widen_ok(buf[u], ok[u], xv);
+            const float mx = vec_max(xv);
+            st[u] = md_fold_lazy(st[u], xv, mx);
+            if (__builtin_amdgcn_ballot_w64(ok[u] && mx >= tw.tau_v) != 0) {
+                const int64_t e0 = head + (b0 + (int64_t)u * TR + tr) * E;
+                tw.template offer<E>(xv, (uint32_t)e0, ok[u]);
+            }
+        }
+        if (tw.qcount >= TK_FLUSH_AT) tw.flush();
+        tw.pull();
+    }
+    tw.flush();
+
+    // merge of the normalizer pairs: wavefront butterflies, then (W > 1)
+    // a fixed-order merge of the row's wavefronts
+    MD md = st[0];
+#pragma unroll
+    for (int u = 1; u < U; ++u) md = md_merge(md, st[u]);
+    md = group_merge<64>(md);
+    uint64_t key = tw.mine;
+    if constexpr (W > 1) {
+        if (lane == 0) wmd[wv] = md;
+        __syncthreads();
+        if (rw != 0) return;
+        const int w0 = wv;  // first wavefront of the row
+        md = wmd[w0];
+#pragma unroll
+        for (int w = 1; w < W; ++w) md = md_merge(md, wmd[w0 + w]);
+        uint64_t e[W];
+#pragma unroll
+        for (int w = 0; w < W; ++w) e[w] = (lane < K) ? region[w0 + w][lane] : 0ull;
+        int found;
+        key = select_topk<W>(e, W, K, &found);
+    }
+    if (lane < K) {
+        const float S = md.s, rd = 1.0f / md.d;
+        vals[row * K + lane] = exp2_hw(__builtin_fmaf(key_value(key), kLog2e, -S)) * rd;
+        idx[row * K + lane] = key_index(key);
+    }
+}
+
+#ifndef OSM_TOPK_U1
+#define OSM_TOPK_U1 8
+#endif
+#ifndef OSM_TOPK_U2
+#define OSM_TOPK_U2 8
+#endif
+#ifndef OSM_TOPK_U4
+#define OSM_TOPK_U4 2
+#endif
+
 hipError_t launch_topk_fused(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V,
-                             int K, int dtype, bool vec, hipStream_t st) {
+                             int K, int dtype, int waves_per_row, hipStream_t st) {
     if (K < 1 || K > TK_KMAX) return hipErrorInvalidValue;
-    dim3 grid((unsigned)N), block(TK_BLOCK);
-    if (dtype == 0) {
-        if (vec)
-            hipLaunchKernelGGL((topk_fused<float, true>), grid, block, 0, st, (const float*)x,
-                               vals, idx, V, K);
+    dim3 block(TK_BLOCK);
+    if (waves_per_row == 1) {
+        constexpr int RB = TK_BLOCK / 64;
+        dim3 grid((unsigned)((N + RB - 1) / RB));
+        if (dtype == 0)
+            hipLaunchKernelGGL((topk_fused<float, 1, OSM_TOPK_U1>), grid, block, 0, st, (const float*)x, vals,
+                               idx, N, V, K);
         else
-            hipLaunchKernelGGL((topk_fused<float, false>), grid, block, 0, st, (const float*)x,
-                               vals, idx, V, K);
+            hipLaunchKernelGGL((topk_fused<bf16_t, 1, OSM_TOPK_U1>), grid, block, 0, st, (const bf16_t*)x,
+                               vals, idx, N, V, K);
+    } else if (waves_per_row == 2) {
+        constexpr int RB = TK_BLOCK / 128;
+        dim3 grid((unsigned)((N + RB - 1) / RB));
+        if (dtype == 0)
+            hipLaunchKernelGGL((topk_fused<float, 2, OSM_TOPK_U2>), grid, block, 0, st,
+                               (const float*)x, vals, idx, N, V, K);
+        else
+            hipLaunchKernelGGL((topk_fused<bf16_t, 2, OSM_TOPK_U2>), grid, block, 0, st,
+                               (const bf16_t*)x, vals, idx, N, V, K);
+    } else if (waves_per_row == 4) {
+        dim3 grid((unsigned)N);
+        if (dtype == 0)
+            hipLaunchKernelGGL((topk_fused<float, 4, OSM_TOPK_U4>), grid, block, 0, st, (const float*)x, vals,
+                               idx, N, V, K);
+        else
+            hipLaunchKernelGGL((topk_fused<bf16_t, 4, OSM_TOPK_U4>), grid, block, 0, st, (const bf16_t*)x,
+                               vals, idx, N, V, K);
     } else {
-        if (vec)
-            hipLaunchKernelGGL((topk_fused<bf16_t, true>), grid, block, 0, st,
-                               (const bf16_t*)x, vals, idx, V, K);
-        else
-            hipLaunchKernelGGL((topk_fused<bf16_t, false>), grid, block, 0, st,
-                               (const bf16_t*)x, vals, idx, V, K);
+        return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }

@@ -22,7 +22,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("softmax_fwd", "softmax_fwd_ex", "softmax_topk", "softmax_topk_dt",
-                 "osm_plan", "osm_status_string"):
+                 "softmax_topk_ex", "osm_plan", "osm_status_string"):
         assert want in names
 
 
@@ -97,6 +97,11 @@ V_, I_ = 0x30000000, 0x40000000
 ])
 def test_softmax_topk_rejects(args):
     assert osm.lib().softmax_topk(*args, None) == osm.EINVAL
+
+
+@pytest.mark.parametrize("kernel,param", [(2, 4), (1, 32), (1, 512), (1, 0), (5, 64)])
+def test_softmax_topk_ex_rejects(kernel, param):
+    assert osm.lib().softmax_topk_ex(X, V_, I_, 4, 10, 5, 0, kernel, param, None) == osm.EINVAL
 
 
 def test_softmax_topk_dt_rejects_unknown_dtype():

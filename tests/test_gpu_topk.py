@@ -19,41 +19,51 @@ def dev():
     return torch.device("cuda:0")
 
 
-def check(x, K, what):
-    vals, idx = osm.softmax_topk(x, K)
+SHAPES = (64, 128, 256)  # lanes per row: one, two or four wavefronts
+
+
+def check(x, K, what, lanes=None):
+    if lanes is None:
+        vals, idx = osm.softmax_topk(x, K)
+    else:
+        vals, idx = osm.softmax_topk(x, K, kernel=osm.KERNEL_ROWS, param=lanes)
     torch.cuda.synchronize()
     v64, z64 = oracle.topk(to_host(x), K, host_dtype(x))
     assert_topk_equal(to_host(vals), to_host(idx), v64, z64, what)
 
 
+@pytest.mark.parametrize("lanes", SHAPES)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_lengths_and_k(dev, dtype):
+def test_lengths_and_k(dev, dtype, lanes):
     for V in (1, 2, 3, 5, 8, 9, 63, 64, 65, 255, 256, 257, 1000, 1001, 4097, 32000, 50001):
         for K in sorted({1, 2, 5, 10, 50, 64, V}):
             if K > V or K > osm.TOPK_KMAX:
                 continue
             N = 23 if V < 10000 else 7
-            print(f"topk dtype={dtype} V={V} K={K}", flush=True)
+            print(f"topk dtype={dtype} lanes={lanes} V={V} K={K}", flush=True)
             x = synth.logits(N, V, sigma=2.0, seed=V * 7 + K, dtype=dtype, device=dev)
-            check(x, K, f"{dtype} V={V} K={K}")
+            check(x, K, f"{dtype} lanes={lanes} V={V} K={K}", lanes)
 
 
+@pytest.mark.parametrize("lanes", SHAPES)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_heavy_ties(dev, dtype):
+def test_heavy_ties(dev, dtype, lanes):
     """Values on a coarse grid: long runs of equal values straddle slot K."""
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     g = torch.Generator(device=dev).manual_seed(4)
     for V in (100, 3000, 40000):
         x = torch.randint(-3, 4, (13, V), generator=g, device=dev).to(tdt) * 0.5
         for K in (1, 5, 17, 64):
-            check(x, K, f"ties {dtype} V={V} K={K}")
+            check(x, K, f"ties {dtype} V={V} K={K}", lanes)
     # every element equal
     x = torch.full((5, 5000), 1.25, dtype=tdt, device=dev)
-    check(x, 64, "all equal")
+    check(x, 64, "all equal", lanes)
+    check(x, 3, "all equal", lanes)
 
 
+@pytest.mark.parametrize("lanes", SHAPES)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_special_values(dev, dtype):
+def test_special_values(dev, dtype, lanes):
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     ninf = float("-inf")
     V = 700
@@ -67,26 +77,36 @@ def test_special_values(dev, dtype):
         base + 1000.0,
     ]).to(tdt).to(dev)
     for K in (1, 3, 5, 10):
-        check(rows, K, f"special {dtype} K={K}")
+        check(rows, K, f"special {dtype} K={K}", lanes)
     # K larger than the finite elements: -inf elements fill in, lowest index first
-    check(rows[3:4], 8, f"-inf fill {dtype}")
+    check(rows[3:4], 8, f"-inf fill {dtype}", lanes)
 
 
-def test_unaligned_rows(dev):
+@pytest.mark.parametrize("lanes", SHAPES)
+def test_unaligned_rows(dev, lanes):
     """x starting off the 16-byte phase (a view into a larger buffer)."""
     buf = synth.logits(1, 37 * 999 + 3, sigma=2.0, seed=8, device=dev)
     x = buf[0, 3:].view(37, 999)
-    check(x, 5, "unaligned x")
+    check(x, 5, "unaligned x", lanes)
     bbuf = synth.logits(1, 21 * 4097 + 5, sigma=2.0, seed=9, dtype="bf16", device=dev)
-    check(bbuf[0, 5:].view(21, 4097), 7, "unaligned bf16 x")
+    check(bbuf[0, 5:].view(21, 4097), 7, "unaligned bf16 x", lanes)
+
+
+def test_batch_not_multiple_of_rows_per_workgroup(dev):
+    """One wavefront per row packs four rows per workgroup: ragged last block."""
+    for N in (1, 2, 3, 5, 1027):
+        x = synth.logits(N, 3001, sigma=2.0, seed=N, device=dev)
+        check(x, 5, f"N={N}", 64)
 
 
 def test_deterministic(dev):
     x = synth.logits(500, 32000, sigma=2.0, seed=10, device=dev)
-    a = osm.softmax_topk(x, 10)
-    b = osm.softmax_topk(x, 10)
-    torch.cuda.synchronize()
-    assert torch.equal(a[1], b[1]) and torch.equal(a[0].view(torch.int32), b[0].view(torch.int32))
+    for lanes in SHAPES:
+        a = osm.softmax_topk(x, 10, kernel=osm.KERNEL_ROWS, param=lanes)
+        b = osm.softmax_topk(x, 10, kernel=osm.KERNEL_ROWS, param=lanes)
+        torch.cuda.synchronize()
+        assert torch.equal(a[1], b[1])
+        assert torch.equal(a[0].view(torch.int32), b[0].view(torch.int32))
 
 
 def test_small_workload_16x1000(dev):
