@@ -29,7 +29,7 @@
 //  * Select.  When the queue fills up, or holds enough entries to be worth
 //    raising tau, the wavefront selects the K largest keys of list + queue:
 //    K rounds of "largest key below the last one taken", each a scan of the
-//    occupied slots (one per lane per 64) and a 6-step butterfly maximum.
+//    occupied slots (one per lane per 64) and two 32-bit butterfly maxima.
 //    Lane k ends holding the k-th key, so the list stays sorted.
 //  * Output.  The normalizer pairs are merged (Eq. 4) and the sorted list
 //    gives v_i = 2^{x_i log2e - s} / d and z_i = index, in key order.  With
@@ -72,25 +72,26 @@ __device__ __forceinline__ float key_value(uint64_t k) {
 
 __device__ __forceinline__ int32_t key_index(uint64_t k) { return (int32_t)(~(uint32_t)k); }
 
-// Largest key over the wavefront (six butterfly steps of md.hpp); every lane
-// gets the same value.
-template <int STEP>
-__device__ __forceinline__ uint64_t key_bfly(uint64_t k) {
-    uint32_t ah, bh, al, bl;
-    bfly_operands<STEP>((uint32_t)(k >> 32), ah, bh);
-    bfly_operands<STEP>((uint32_t)k, al, bl);
-    const uint64_t a = ((uint64_t)ah << 32) | al, b = ((uint64_t)bh << 32) | bl;
-    return a > b ? a : b;
+// Largest key over the wavefront; every lane gets the same value.  Two
+// 32-bit butterfly maxima (md.hpp steps, DPP-fused where possible): first
+// over the value words, then over the index words of the lanes holding that
+// value word.  Keys are distinct, so the pair identifies the largest key.
+template <int STEP = 0>
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    if constexpr (STEP < 6) {
+        uint32_t a, b;
+        bfly_operands<STEP>(v, a, b);
+        return wave_max_u32<STEP + 1>(a > b ? a : b);
+    } else {
+        return v;
+    }
 }
 
 __device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
-    k = key_bfly<0>(k);
-    k = key_bfly<1>(k);
-    k = key_bfly<2>(k);
-    k = key_bfly<3>(k);
-    k = key_bfly<4>(k);
-    k = key_bfly<5>(k);
-    return k;
+    const uint32_t hi = (uint32_t)(k >> 32), lo = (uint32_t)k;
+    const uint32_t mh = wave_max_u32(hi);
+    const uint32_t ml = wave_max_u32(hi == mh ? lo : 0u);
+    return ((uint64_t)mh << 32) | ml;
 }
 
 // The same 64-bit value on every lane, taken from lane `src` (uniform).
@@ -339,15 +340,27 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
             }
             if (k == K) tw.raise_tau((make_key(last, 0u) & 0xFFFFFFFF00000000ull) - 1);
         }
+        float mxs[U];
+        float lane_mx = -__builtin_inff();
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             float xv[E];
             widen_ok(buf[u], ok[u], xv);
-            const float mx = vec_max(xv);
-            st[u] = md_fold_lazy(st[u], xv, mx);
-            if (__builtin_amdgcn_ballot_w64(ok[u] && mx >= tw.tau_v) != 0) {
-                const int64_t e0 = head + (b0 + (int64_t)u * TR + tr) * E;
-                tw.template offer<E>(xv, (uint32_t)e0, ok[u]);
+            mxs[u] = vec_max(xv);
+            lane_mx = fmaxf(lane_mx, mxs[u]);
+            st[u] = md_fold_lazy(st[u], xv, mxs[u]);
+        }
+        // one test per step; per-vector tests only when some lane may hold
+        // a candidate
+        if (__builtin_amdgcn_ballot_w64(lane_mx >= tw.tau_v) != 0) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (__builtin_amdgcn_ballot_w64(ok[u] && mxs[u] >= tw.tau_v) != 0) {
+                    float xv[E];
+                    widen_ok(buf[u], ok[u], xv);
+                    const int64_t e0 = head + (b0 + (int64_t)u * TR + tr) * E;
+                    tw.template offer<E>(xv, (uint32_t)e0, ok[u]);
+                }
             }
         }
         if (tw.qcount >= TK_FLUSH_AT) tw.flush();
@@ -383,8 +396,14 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     }
 }
 
+// 16-byte vectors per lane per step, by shape and element type: enough
+// loads in flight per wavefront without pushing the register count (and so
+// the occupancy) down; bfloat16 vectors widen to twice the registers.
 #ifndef OSM_TOPK_U1
 #define OSM_TOPK_U1 8
+#endif
+#ifndef OSM_TOPK_U1B
+#define OSM_TOPK_U1B 4
 #endif
 #ifndef OSM_TOPK_U2
 #define OSM_TOPK_U2 8
@@ -404,7 +423,7 @@ hipError_t launch_topk_fused(const void* x, float* vals, int32_t* idx, int64_t N
             hipLaunchKernelGGL((topk_fused<float, 1, OSM_TOPK_U1>), grid, block, 0, st, (const float*)x, vals,
                                idx, N, V, K);
         else
-            hipLaunchKernelGGL((topk_fused<bf16_t, 1, OSM_TOPK_U1>), grid, block, 0, st, (const bf16_t*)x,
+            hipLaunchKernelGGL((topk_fused<bf16_t, 1, OSM_TOPK_U1B>), grid, block, 0, st, (const bf16_t*)x,
                                vals, idx, N, V, K);
     } else if (waves_per_row == 2) {
         constexpr int RB = TK_BLOCK / 128;
@@ -413,7 +432,7 @@ hipError_t launch_topk_fused(const void* x, float* vals, int32_t* idx, int64_t N
             hipLaunchKernelGGL((topk_fused<float, 2, OSM_TOPK_U2>), grid, block, 0, st,
                                (const float*)x, vals, idx, N, V, K);
         else
-            hipLaunchKernelGGL((topk_fused<bf16_t, 2, OSM_TOPK_U2>), grid, block, 0, st,
+            hipLaunchKernelGGL((topk_fused<bf16_t, 2, OSM_TOPK_U1B>), grid, block, 0, st,
                                (const bf16_t*)x, vals, idx, N, V, K);
     } else if (waves_per_row == 4) {
         dim3 grid((unsigned)N);
