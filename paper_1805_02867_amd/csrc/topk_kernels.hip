@@ -299,65 +299,55 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     // wavefront-wide queue operations see all 64 lanes
     const u32x4 ninf = (E == 4) ? u32x4{0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u}
                                 : u32x4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
-    // Loads are unconditional (an index past the row is clamped to the last
-    // vector and its data masked afterwards): a load under a branch would
-    // stop the compiler from counting outstanding loads and make it wait for
-    // all of them.
-    const int64_t vlast = nvec > 0 ? nvec - 1 : 0;
-    auto load = [&](u32x4 (&buf)[U], bool (&ok)[U], int64_t b0) {
+    // Full steps (every lane holds U whole vectors) run as a software
+    // pipeline over two register buffers: the loads of step t + 1 are issued
+    // before step t is processed.  Their addresses are a per-lane pointer plus
+    // immediate offsets, so the compiler waits only for the buffer it is
+    // about to use.  The remaining vectors (fewer than a step) form one last
+    // step with indices clamped into the row and masked after loading.
+    const int64_t nfull = nvec / STEP;
+    const u32x4* lp = vb + tr;  // this lane's first vector
+    auto load_full = [&](u32x4 (&buf)[U], int64_t sidx) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t vi = b0 + (int64_t)u * TR + tr;
-            ok[u] = vi < nvec;
-            buf[u] = __builtin_nontemporal_load(vb + (vi < nvec ? vi : vlast));
-        }
+        for (int u = 0; u < U; ++u) buf[u] = __builtin_nontemporal_load(lp + sidx * STEP + u * TR);
+        // keep the scheduler from hoisting the next step's work above these
+        // loads (that would make it wait for the previous buffer first)
+        __builtin_amdgcn_sched_barrier(0);
     };
-    auto widen_ok = [&](u32x4 q, bool ok, float (&xv)[E]) { widen<T>(ok ? q : ninf, xv); };
-
-    u32x4 buf[U];
-    bool ok[U];
-    for (int64_t b0 = 0; b0 < nvec; b0 += STEP) {
-        load(buf, ok, b0);
-        if (b0 == 0) {
-            // Bootstrap: the K-th largest distinct value among the lanes'
-            // first-step maxima bounds the row's K-th value from below; keys
-            // >= (that value, any index) are kept, i.e. keys > (value key with
-            // index word 0) - 1.
-            float lm = -__builtin_inff();
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                float xv[E];
-                widen_ok(buf[u], ok[u], xv);
-                lm = fmaxf(lm, vec_max(xv));
-            }
-            float last = __builtin_inff();
-            int k = 0;
-            for (; k < K; ++k) {
-                float c = (lm < last) ? lm : -__builtin_inff();
-                c = group_max<64>(c);
-                if (!(c > -__builtin_inff())) break;
-                last = c;
-            }
-            if (k == K) tw.raise_tau((make_key(last, 0u) & 0xFFFFFFFF00000000ull) - 1);
+    // Bootstrap: the K-th largest distinct value among the lanes' maxima
+    // over the first step bounds the row's K-th value from below; keys
+    // >= (that value, any index) are kept, i.e. keys > (value key with index
+    // word 0) - 1.
+    auto bootstrap = [&](const float (&lm)[1]) {
+        float last = __builtin_inff();
+        int k = 0;
+        for (; k < K; ++k) {
+            float c = (lm[0] < last) ? lm[0] : -__builtin_inff();
+            c = group_max<64>(c);
+            if (!(c > -__builtin_inff())) break;
+            last = c;
         }
+        if (k == K) tw.raise_tau((make_key(last, 0u) & 0xFFFFFFFF00000000ull) - 1);
+    };
+    // One step: fold every vector, then (one test per step) offer the vectors
+    // that may hold a candidate.
+    auto step = [&](const u32x4 (&buf)[U], const bool (&ok)[U], int64_t b0, bool masked) {
         float mxs[U];
         float lane_mx = -__builtin_inff();
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             float xv[E];
-            widen_ok(buf[u], ok[u], xv);
+            widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
             mxs[u] = vec_max(xv);
             lane_mx = fmaxf(lane_mx, mxs[u]);
             st[u] = md_fold_lazy(st[u], xv, mxs[u]);
         }
-        // one test per step; per-vector tests only when some lane may hold
-        // a candidate
         if (__builtin_amdgcn_ballot_w64(lane_mx >= tw.tau_v) != 0) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 if (__builtin_amdgcn_ballot_w64(ok[u] && mxs[u] >= tw.tau_v) != 0) {
                     float xv[E];
-                    widen_ok(buf[u], ok[u], xv);
+                    widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
                     const int64_t e0 = head + (b0 + (int64_t)u * TR + tr) * E;
                     tw.template offer<E>(xv, (uint32_t)e0, ok[u]);
                 }
@@ -365,6 +355,53 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
         }
         if (tw.qcount >= TK_FLUSH_AT) tw.flush();
         tw.pull();
+    };
+    auto lane_max_of = [&](const u32x4 (&buf)[U], const bool (&ok)[U], bool masked) {
+        float lm = -__builtin_inff();
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            float xv[E];
+            widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
+            lm = fmaxf(lm, vec_max(xv));
+        }
+        return lm;
+    };
+
+    bool all_ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) all_ok[u] = true;
+    bool booted = false;
+    if (nfull > 0) {
+        u32x4 ba[U], bb[U];
+        load_full(ba, 0);
+        const float lm[1] = {lane_max_of(ba, all_ok, false)};
+        bootstrap(lm);
+        booted = true;
+        int64_t j = 0;
+        for (; j + 2 <= nfull; j += 2) {
+            load_full(bb, j + 1);
+            step(ba, all_ok, j * STEP, false);
+            load_full(ba, (j + 2 < nfull) ? j + 2 : j + 1);  // stays inside the row
+            step(bb, all_ok, (j + 1) * STEP, false);
+        }
+        if (j < nfull) step(ba, all_ok, j * STEP, false);
+    }
+    if (nfull * STEP < nvec) {
+        // last, partial step: clamped indices, masked lanes
+        const int64_t b0 = nfull * STEP, vlast = nvec - 1;
+        u32x4 bt[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t vi = b0 + (int64_t)u * TR + tr;
+            ok[u] = vi < nvec;
+            bt[u] = __builtin_nontemporal_load(vb + (vi < nvec ? vi : vlast));
+        }
+        if (!booted) {
+            const float lm[1] = {lane_max_of(bt, ok, true)};
+            bootstrap(lm);
+        }
+        step(bt, ok, b0, true);
     }
     tw.flush();
 
@@ -400,13 +437,13 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
 // loads in flight per wavefront without pushing the register count (and so
 // the occupancy) down; bfloat16 vectors widen to twice the registers.
 #ifndef OSM_TOPK_U1
-#define OSM_TOPK_U1 8
+#define OSM_TOPK_U1 4
 #endif
 #ifndef OSM_TOPK_U1B
-#define OSM_TOPK_U1B 4
+#define OSM_TOPK_U1B 2
 #endif
 #ifndef OSM_TOPK_U2
-#define OSM_TOPK_U2 8
+#define OSM_TOPK_U2 4
 #endif
 #ifndef OSM_TOPK_U4
 #define OSM_TOPK_U4 2
