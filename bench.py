@@ -16,6 +16,7 @@ naive and safe modes are timed on the same batch after the steps, for the
 paper's memory-access comparison.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+       python bench.py --sweep FILE   (every workload shape and V sweep)
 """
 from __future__ import annotations
 
@@ -100,6 +101,78 @@ def copy_probe():
         f"{2 * n * 4 / (median(t) * 1e-3) / 1e9:.0f} GB/s (read+write)")
 
 
+def sweep(path: str):
+    """Every workload shape (and the paper's V sweeps at batch 4000 and 10):
+    one JSON record per (shape, mode) into `path`.  Each record is the median
+    over 10 timed batches of back-to-back launches (enough launches per
+    batch that each batch runs >= ~1 ms), so small shapes are measured as a
+    stream of calls rather than one launch latency."""
+    import torch
+    import paper_1805_02867_amd as osm
+    from paper_1805_02867_amd import synth
+    stream = torch.cuda.current_stream()
+    out = open(path, "w")
+
+    def run(fn, est_us):
+        reps = max(1, int(1000.0 / max(est_us, 1.0)))
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(10):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(reps):
+                fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e3 / reps)
+        return median(ts)
+
+    def emit(rec):
+        out.write(json.dumps(rec) + "\n")
+        out.flush()
+        log(json.dumps(rec))
+
+    cases = [  # (name, N, V, dtype, sigma, extra)
+        ("softmax_topk_16x1000_f32", 16, 1000, "f32", 1.0, {}),
+        ("softmax_4000x32000_f32_shift", 4000, 32000, "f32", 2.0, {"shift_frac": 0.01}),
+        ("softmax_10x1e6_f32", 10, 1_000_000, "f32", 3.0, {}),
+        ("topk_4000x50000_f32_ties", 4000, 50000, "f32", 2.0, {"tie_frac": 0.01}),
+        ("softmax_topk_32768x128256_bf16", 32768, 128256, "bf16", 4.0, {}),
+    ]
+    for V in (35, 100, 300, 1000, 3000, 4000, 10000, 25000, 100000, 500000):
+        cases.append((f"sweep_4000x{V}_f32", 4000, V, "f32", 2.0, {}))
+    for V in (1000, 10000, 100000, 1000000, 15000000):
+        cases.append((f"sweep_10x{V}_f32", 10, V, "f32", 2.0, {}))
+    topk_k = {"softmax_topk_16x1000_f32": (5,), "softmax_4000x32000_f32_shift": (5, 10),
+              "topk_4000x50000_f32_ties": (5, 10), "softmax_topk_32768x128256_bf16": (5, 50)}
+    for name, N, V, dt, sg, extra in cases:
+        x = synth.logits(N, V, sigma=sg, seed=0, dtype=dt, device="cuda", **extra)
+        es = 2 if dt == "bf16" else 4
+        y = torch.empty_like(x)
+        est = 12.0 * N * V / 6e3 / 1e3  # us at ~6 TB/s
+        for mode, acc in (("online", 3), ("safe", 4), ("naive", 3)):
+            us = run(lambda m=mode: osm.softmax_fwd(x, y, mode=m), est)
+            emit({"workload": name, "op": f"softmax_{mode}", "N": N, "V": V, "dtype": dt,
+                  "plan": list(osm.plan(N, V, x.dtype, mode)), "us": round(us, 2),
+                  "GBps": round(acc * es * N * V / us / 1e3, 1),
+                  "elements_per_s": round(N * V / us * 1e6, 1), "rows_per_s": round(N / us * 1e6, 1)})
+        del y
+        for K in topk_k.get(name, (5,)):
+            if K > V:
+                continue
+            vals = torch.empty((N, K), dtype=torch.float32, device="cuda")
+            idx = torch.empty((N, K), dtype=torch.int32, device="cuda")
+            us = run(lambda: osm.softmax_topk(x, K, vals, idx), est / 3)
+            emit({"workload": name, "op": f"topk_fused_k{K}", "N": N, "V": V, "dtype": dt,
+                  "us": round(us, 2), "GBps": round((es * N * V + 8 * N * K) / us / 1e3, 1),
+                  "elements_per_s": round(N * V / us * 1e6, 1), "rows_per_s": round(N / us * 1e6, 1)})
+        del x
+        torch.cuda.empty_cache()
+    out.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,6 +181,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--compare-reps", type=int, default=20)
+    ap.add_argument("--sweep", metavar="FILE", help="time every workload shape and the V "
+                    "sweeps; one JSON record per line into FILE")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
@@ -124,6 +199,9 @@ def main():
     osm.lib()  # fail loudly if the HIP library is not built
     if args.copy_probe:
         copy_probe()
+        return
+    if args.sweep:
+        sweep(args.sweep)
         return
 
     dev = torch.device("cuda:0")

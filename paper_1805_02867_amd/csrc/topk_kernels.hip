@@ -52,7 +52,14 @@ constexpr int TK_BLOCK = 256;
 constexpr int TK_KMAX = 64;            // largest supported K (one list slot per lane)
 constexpr int TK_REGION = 320;         // list + queue slots per wavefront
 constexpr int TK_PER_LANE = TK_REGION / 64;
-constexpr int TK_FLUSH_AT = 32;        // select early once the queue holds this many
+// Select early once the queue holds this many (per K): small K profits from
+// a threshold refreshed often; large K pays K rounds per selection, so it
+// waits until the queue is nearly full.
+__device__ __forceinline__ int flush_at(int K) {
+    const int f = 4 * K > 32 ? 4 * K : 32;
+    const int cap = TK_REGION - K - 64;
+    return f < cap ? f : cap;
+}
 
 static_assert(TK_REGION % 64 == 0, "region must split evenly over 64 lanes");
 static_assert(TK_REGION - TK_KMAX >= 64, "the queue must take a full wavefront");
@@ -306,6 +313,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     // about to use.  The remaining vectors (fewer than a step) form one last
     // step with indices clamped into the row and masked after loading.
     const int64_t nfull = nvec / STEP;
+    const int fa = flush_at(K);
     const u32x4* lp = vb + tr;  // this lane's first vector
     auto load_full = [&](u32x4 (&buf)[U], int64_t sidx) {
 #pragma unroll
@@ -353,7 +361,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
                 }
             }
         }
-        if (tw.qcount >= TK_FLUSH_AT) tw.flush();
+        if (tw.qcount >= fa) tw.flush();
         tw.pull();
     };
     auto lane_max_of = [&](const u32x4 (&buf)[U], const bool (&ok)[U], bool masked) {
