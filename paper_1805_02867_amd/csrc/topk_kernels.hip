@@ -52,13 +52,16 @@ constexpr int TK_BLOCK = 256;
 constexpr int TK_KMAX = 64;            // largest supported K (one list slot per lane)
 constexpr int TK_REGION = 320;         // list + queue slots per wavefront
 constexpr int TK_PER_LANE = TK_REGION / 64;
-// Select early once the queue holds this many (per K): small K profits from
-// a threshold refreshed often; large K pays K rounds per selection, so it
-// waits until the queue is nearly full.
+// Selections with more than this many rounds use the sorting network.
+constexpr int TK_ROUNDS_MAX = 16;
+
+// Select early once the queue holds this many (per K): a threshold refreshed
+// often saves candidates; the K-round selection costs K rounds, so its
+// trigger grows with K, while the sorting-network selection (large K) costs
+// one pass per 64 queued keys and runs at one full chunk.
 __device__ __forceinline__ int flush_at(int K) {
-    const int f = 4 * K > 32 ? 4 * K : 32;
-    const int cap = TK_REGION - K - 64;
-    return f < cap ? f : cap;
+    if (K > TK_ROUNDS_MAX) return 64;
+    return 4 * K > 32 ? 4 * K : 32;
 }
 
 static_assert(TK_REGION % 64 == 0, "region must split evenly over 64 lanes");
@@ -99,6 +102,95 @@ __device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
     const uint32_t mh = wave_max_u32(hi);
     const uint32_t ml = wave_max_u32(hi == mh ? lo : 0u);
     return ((uint64_t)mh << 32) | ml;
+}
+
+// ----------------------------------------------------------------- sorting
+// Value of lane (lane ^ J) for the sorting networks: DPP quad permutations
+// for 1 and 2, the LDS-crossbar swizzle for 4 and 8, and for 16 and 32 the
+// operand of the permlane swap pair that came from the other row / half
+// (after a 16-lane swap, lanes of even rows hold their partner's value in
+// the second result and lanes of odd rows in the first; likewise for the
+// 32-lane halves).
+template <int J>
+__device__ __forceinline__ uint32_t xor_partner(uint32_t v) {
+    if constexpr (J == 1) {
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+    } else if constexpr (J == 2) {
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+    } else if constexpr (J == 4 || J == 8) {
+        return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, (J << 10) | 0x1F);
+    } else if constexpr (J == 16) {
+        auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return (__lane_id() & 16) ? p[0] : p[1];
+    } else {
+        static_assert(J == 32, "xor partner distance must be a power of two below 64");
+        auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return (__lane_id() & 32) ? p[0] : p[1];
+    }
+}
+
+template <int J>
+__device__ __forceinline__ uint64_t xor_partner_key(uint64_t k) {
+    return ((uint64_t)xor_partner<J>((uint32_t)(k >> 32)) << 32) | xor_partner<J>((uint32_t)k);
+}
+
+// One compare-exchange stage: the lower lane of each pair keeps the larger
+// key when `desc_block` holds, the smaller one otherwise (and the upper lane
+// the other one).
+template <int J>
+__device__ __forceinline__ uint64_t cx_stage(uint64_t v, bool desc_block) {
+    const uint64_t p = xor_partner_key<J>(v);
+    const bool lower = (__lane_id() & J) == 0;
+    const bool keep_max = lower == desc_block;
+    const bool take = keep_max ? (p > v) : (p < v);
+    return take ? p : v;
+}
+
+// Bitonic sort of one key per lane over the wavefront: lane 0 ends with the
+// largest key.
+template <int KB, int J>
+__device__ __forceinline__ uint64_t bitonic_stage_run(uint64_t v) {
+    if constexpr (J >= 1) {
+        const bool desc_block = (__lane_id() & KB) == 0;  // KB = 64: the whole wave descends
+        v = cx_stage<J>(v, desc_block);
+        return bitonic_stage_run<KB, J / 2>(v);
+    } else {
+        return v;
+    }
+}
+
+__device__ __forceinline__ uint64_t sort_desc(uint64_t v) {
+    v = bitonic_stage_run<2, 1>(v);
+    v = bitonic_stage_run<4, 2>(v);
+    v = bitonic_stage_run<8, 4>(v);
+    v = bitonic_stage_run<16, 8>(v);
+    v = bitonic_stage_run<32, 16>(v);
+    v = bitonic_stage_run<64, 32>(v);
+    return v;
+}
+
+// Sort of a bitonic sequence (one key per lane): lane 0 ends with the largest.
+__device__ __forceinline__ uint64_t bitonic_merge_desc(uint64_t v) {
+    return bitonic_stage_run<64, 32>(v);
+}
+
+// Key of lane 63 - lane (xor 63 = mirror within 16 lanes, then xor 16, xor 32).
+__device__ __forceinline__ uint64_t reverse_lanes(uint64_t k) {
+    uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(k >> 32), 0x140, 0xF,
+                                                       0xF, false);
+    uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)k, 0x140, 0xF, 0xF,
+                                                       false);
+    hi = xor_partner<32>(xor_partner<16>(hi));
+    lo = xor_partner<32>(xor_partner<16>(lo));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Top 64 keys of (sorted list `cur`, one key per lane, lane 0 largest) and
+// (64 more keys, any order), sorted the same way.
+__device__ __forceinline__ uint64_t merge_chunk(uint64_t cur, uint64_t q) {
+    q = reverse_lanes(sort_desc(q));         // ascending across lanes
+    const uint64_t m = cur > q ? cur : q;     // top 64 of the union, a bitonic sequence
+    return bitonic_merge_desc(m);
 }
 
 // The same 64-bit value on every lane, taken from lane `src` (uniform).
@@ -156,17 +248,31 @@ struct TopkWave {
     }
 
     // list + queue -> new list; resets the queue; raises (and publishes) tau.
+    // Small K: K rounds of a wavefront maximum.  Large K: the queue in chunks
+    // of 64 keys, each sorted and merged into the sorted list (cost
+    // independent of K).
     __device__ __forceinline__ void flush() {
         const int lane = __lane_id();
-        const int used = K + qcount;
-        const int rows = (used + 63) >> 6;
-        wave_sync();
-        uint64_t e[TK_PER_LANE];
-#pragma unroll
-        for (int j = 0; j < TK_PER_LANE; ++j)
-            e[j] = (j < rows && lane + 64 * j < used) ? region[lane + 64 * j] : 0ull;
         int found;
-        mine = select_topk<TK_PER_LANE>(e, rows, K, &found);
+        wave_sync();
+        if (K <= TK_ROUNDS_MAX) {
+            const int used = K + qcount;
+            const int rows = (used + 63) >> 6;
+            uint64_t e[TK_PER_LANE];
+#pragma unroll
+            for (int j = 0; j < TK_PER_LANE; ++j)
+                e[j] = (j < rows && lane + 64 * j < used) ? region[lane + 64 * j] : 0ull;
+            mine = select_topk<TK_PER_LANE>(e, rows, K, &found);
+        } else {
+            uint64_t cur = lane < K ? region[lane] : 0ull;  // sorted list
+            for (int c = 0; c < qcount; c += 64) {
+                const uint64_t q = c + lane < qcount ? region[K + c + lane] : 0ull;
+                cur = merge_chunk(cur, q);
+            }
+            mine = lane < K ? cur : 0ull;
+            found = (mine != 0) ? lane + 1 : 0;
+            found = (int)wave_max_u32((uint32_t)found);
+        }
         wave_sync();
         if (lane < K) region[lane] = mine;
         wave_sync();
@@ -326,16 +432,27 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     // over the first step bounds the row's K-th value from below; keys
     // >= (that value, any index) are kept, i.e. keys > (value key with index
     // word 0) - 1.
+    // (Large K: the K-th of the lanes' maxima, counted with multiplicity,
+    // read off a sort; still a lower bound, as the lanes hold distinct
+    // elements.)
     auto bootstrap = [&](const float (&lm)[1]) {
-        float last = __builtin_inff();
-        int k = 0;
-        for (; k < K; ++k) {
-            float c = (lm[0] < last) ? lm[0] : -__builtin_inff();
-            c = group_max<64>(c);
-            if (!(c > -__builtin_inff())) break;
-            last = c;
+        if (K <= TK_ROUNDS_MAX) {
+            float last = __builtin_inff();
+            int k = 0;
+            for (; k < K; ++k) {
+                float c = (lm[0] < last) ? lm[0] : -__builtin_inff();
+                c = group_max<64>(c);
+                if (!(c > -__builtin_inff())) break;
+                last = c;
+            }
+            if (k == K) tw.raise_tau((make_key(last, 0u) & 0xFFFFFFFF00000000ull) - 1);
+        } else {
+            // keys with the lane as a stand-in index: only their value words are used
+            const uint64_t srt = sort_desc(lm[0] > -__builtin_inff()
+                                               ? make_key(lm[0], (uint32_t)lane) : 0ull);
+            const uint64_t kth = read_lane_key(srt, K - 1);
+            if (kth != 0) tw.raise_tau((kth & 0xFFFFFFFF00000000ull) - 1);
         }
-        if (k == K) tw.raise_tau((make_key(last, 0u) & 0xFFFFFFFF00000000ull) - 1);
     };
     // One step: fold every vector, then (one test per step) offer the vectors
     // that may hold a candidate.
