@@ -70,15 +70,41 @@ enum osm_status {
     OSM_ENOMEM = 4        /* scratch allocation failed */
 };
 
-/* Kernel families for softmax_fwd_ex. */
+/* Kernel families for softmax_fwd_ex, softmax_topk_ex and softmax_topk_algo. */
 enum osm_kernel {
-    OSM_KERNEL_AUTO = 0,  /* what softmax_fwd uses */
-    OSM_KERNEL_ROWS = 1,  /* param = lanes per row: 4, 8, 16, 32 (several rows
-                             per wavefront), 64 (a row per wavefront) or
-                             128, 256, 512, 1024 (a row per workgroup) */
-    OSM_KERNEL_SPLIT = 2  /* param = chunks per row S >= 1: several workgroups
-                             per row, partial pairs merged through a scratch
-                             array (stream-ordered allocation) */
+    OSM_KERNEL_AUTO = 0,  /* what the plain entry points use */
+    OSM_KERNEL_ROWS = 1,  /* param = lanes per row.  Softmax: 4, 8, 16, 32
+                             (several rows per wavefront), 64 (a row per
+                             wavefront) or 128, 256, 512, 1024 (a row per
+                             workgroup).  Top-k: 64, 128 or 256 (one, two or
+                             four wavefronts per row). */
+    OSM_KERNEL_SPLIT = 2  /* param = chunks per row S >= 1: a workgroup per
+                             chunk; per-chunk normalizer pairs (and, for
+                             top-k, per-chunk top-k keys) are merged in a
+                             second kernel through a scratch array
+                             (stream-ordered allocation) */
+};
+
+/* Softmax + top-k algorithms (Section 4, and the comparisons of Section 5.2):
+ *  OSM_TOPK_ONLINE_FUSED  : Alg. 4 -- online pair and top-k in one pass, one
+ *                           load per element.  What softmax_topk uses.
+ *  OSM_TOPK_SAFE_FUSED    : a maximum pass, then the normalizer (with that
+ *                           maximum) and top-k in one pass: two loads per
+ *                           element.
+ *  OSM_TOPK_SAFE_UNFUSED  : safe softmax (Alg. 2) writes y, then a separate
+ *                           top-k over y: five accesses per element.
+ *  OSM_TOPK_ONLINE_UNFUSED: online softmax (Alg. 3) writes y, then top-k over
+ *                           y: four accesses per element.
+ *  OSM_TOPK_VALUES        : top-k of x itself, no softmax (vals = x[z]).
+ * The fused algorithms select on x; the unfused ones select on the stored y
+ * (Eq. 5), so where distinct inputs round to equal outputs (mostly bfloat16
+ * y) their ties go to the lower index among equal y. */
+enum osm_topk_algo {
+    OSM_TOPK_ONLINE_FUSED = 0,
+    OSM_TOPK_SAFE_FUSED = 1,
+    OSM_TOPK_SAFE_UNFUSED = 2,
+    OSM_TOPK_ONLINE_UNFUSED = 3,
+    OSM_TOPK_VALUES = 4
 };
 
 /* Largest K accepted by the top-k entry points. */
@@ -117,17 +143,49 @@ OSM_API int softmax_topk(const float* x, float* vals, int32_t* idx, int64_t N, i
 OSM_API int softmax_topk_dt(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
                     int dtype, hipStream_t stream);
 
-/* softmax_topk_dt with an explicit kernel shape: kernel OSM_KERNEL_AUTO (what
- * softmax_topk_dt uses; param ignored) or OSM_KERNEL_ROWS with param = lanes
- * per row: 64, 128 or 256 (one, two or four wavefronts per row).  Results
- * are identical across shapes except for binary32 rounding of vals.
- * Errors: as softmax_topk_dt, plus OSM_EINVAL for another kernel or param. */
+/* softmax_topk_dt with an explicit kernel: OSM_KERNEL_AUTO (what
+ * softmax_topk_dt uses; param ignored), OSM_KERNEL_ROWS with param = lanes
+ * per row: 64, 128 or 256 (one, two or four wavefronts per row), or
+ * OSM_KERNEL_SPLIT with param = chunks per row (clamped so that every chunk
+ * starts inside the row).  Indices are identical across kernels; vals agree
+ * within binary32 rounding of the reduction tree.
+ * Errors: as softmax_topk_dt, plus OSM_EINVAL for another kernel or param,
+ * or N * S >= 2^31 chunks; OSM_ENOMEM if the split scratch (N * S * (8K + 8)
+ * bytes) cannot be allocated. */
 OSM_API int softmax_topk_ex(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V,
                             int K, int dtype, int kernel, int64_t param, hipStream_t stream);
+
+/* Softmax + top-k by any osm_topk_algo, with an explicit kernel for the
+ * top-k pass (kernel and param as in softmax_topk_ex; the two-wavefront
+ * shape, param 128, exists for OSM_TOPK_ONLINE_FUSED only; the softmax pass
+ * of the unfused algorithms uses what softmax_fwd uses).
+ * y: N*V elements of dtype, written with the softmax for the unfused
+ * algorithms (must not overlap x, vals or idx); ignored (may be NULL) by the
+ * others.  vals: binary32; for the unfused algorithms and OSM_TOPK_VALUES
+ * they are the selected elements of y (resp. x), widened exactly.
+ * Errors: as softmax_topk_ex, plus OSM_EINVAL for an unknown algo or a
+ * missing / misaligned / overlapping y where one is needed. */
+OSM_API int softmax_topk_algo(const void* x, void* y, float* vals, int32_t* idx, int64_t N,
+                              int64_t V, int K, int dtype, int algo, int kernel, int64_t param,
+                              hipStream_t stream);
+
+/* Top-k of the elements themselves, row by row (the top-k of Eq. 5 applied
+ * to x): z = the K indices of the largest x, larger first, equal values in
+ * increasing index order; vals = x[z] widened to binary32 (-0.0 is returned
+ * as +0.0).  NaN elements are never selected; a row with fewer than K
+ * non-NaN elements gets idx -1 and NaN vals in the missing places.
+ * Errors: as softmax_topk_dt. */
+OSM_API int topk_fwd(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
+                     int dtype, hipStream_t stream);
 
 /* Kernel family and parameter softmax_fwd would use for this shape on the
  * current device.  Errors: OSM_EINVAL for bad sizes, dtype or null outputs. */
 OSM_API int osm_plan(int64_t N, int64_t V, int dtype, int mode, int* kernel, int64_t* param);
+
+/* Kernel family and parameter the top-k entry points would use for this
+ * shape on the current device.  Errors: OSM_EINVAL for bad sizes, dtype, K
+ * or null outputs. */
+OSM_API int osm_topk_plan(int64_t N, int64_t V, int dtype, int K, int* kernel, int64_t* param);
 
 /* Static description of a status code (never NULL). */
 OSM_API const char* osm_status_string(int status);

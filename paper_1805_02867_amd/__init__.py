@@ -19,6 +19,11 @@ NAIVE, SAFE, ONLINE = 0, 1, 2
 KERNEL_AUTO, KERNEL_ROWS, KERNEL_SPLIT = 0, 1, 2
 OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM = 0, 1, 2, 3, 4
 TOPK_KMAX = 64
+TOPK_ONLINE_FUSED, TOPK_SAFE_FUSED, TOPK_SAFE_UNFUSED, TOPK_ONLINE_UNFUSED, TOPK_VALUES = range(5)
+TOPK_ALGOS = {"online_fused": TOPK_ONLINE_FUSED, "safe_fused": TOPK_SAFE_FUSED,
+              "safe_unfused": TOPK_SAFE_UNFUSED, "online_unfused": TOPK_ONLINE_UNFUSED,
+              "values": TOPK_VALUES}
+UNFUSED = (TOPK_SAFE_UNFUSED, TOPK_ONLINE_UNFUSED)
 
 MODES = {"naive": NAIVE, "safe": SAFE, "online": ONLINE}
 _DTYPES = {torch.float32: F32, torch.bfloat16: BF16}
@@ -52,6 +57,12 @@ def lib() -> ctypes.CDLL:
     L.softmax_topk_dt.restype = i32
     L.softmax_topk_ex.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, i64, vp]
     L.softmax_topk_ex.restype = i32
+    L.softmax_topk_algo.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, i32, i64, vp]
+    L.softmax_topk_algo.restype = i32
+    L.topk_fwd.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
+    L.topk_fwd.restype = i32
+    L.osm_topk_plan.argtypes = [i64, i64, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i64)]
+    L.osm_topk_plan.restype = i32
     L.osm_plan.argtypes = [i64, i64, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i64)]
     L.osm_plan.restype = i32
     L.osm_status_string.argtypes = [i32]
@@ -116,13 +127,7 @@ def softmax_fwd(x: torch.Tensor, y: torch.Tensor | None = None, mode="online",
     return y
 
 
-def softmax_topk(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,
-                 idx: torch.Tensor | None = None, stream=None, kernel: int = KERNEL_AUTO,
-                 param: int = 0):
-    """(vals, idx) = fused softmax + top-k per row via ``softmax_topk``
-    (binary32 rows), ``softmax_topk_dt`` (bfloat16 rows) or, with an explicit
-    kernel shape, ``softmax_topk_ex``."""
-    N, V = _batch(x)
+def _topk_outputs(x, N, K, vals, idx):
     if vals is None:
         vals = torch.empty((N, K), dtype=torch.float32, device=x.device)
     if idx is None:
@@ -131,22 +136,79 @@ def softmax_topk(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,
         if (t.dtype != dt or not t.is_contiguous() or t.numel() != N * K
                 or t.device != x.device):
             raise ValueError(f"{nm} must be a contiguous {dt} tensor of N*K elements on x's device")
-    if kernel != KERNEL_AUTO:
+    return vals, idx
+
+
+def _algo(algo) -> int:
+    if isinstance(algo, str):
+        if algo not in TOPK_ALGOS:
+            raise ValueError(f"algo must be one of {sorted(TOPK_ALGOS)}")
+        return TOPK_ALGOS[algo]
+    return int(algo)
+
+
+def softmax_topk(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,
+                 idx: torch.Tensor | None = None, stream=None, kernel: int = KERNEL_AUTO,
+                 param: int = 0, algo="online_fused", y: torch.Tensor | None = None):
+    """(vals, idx) = softmax + top-k per row.
+
+    The default (Alg. 4, one pass) goes through ``softmax_topk`` (binary32
+    rows), ``softmax_topk_dt`` (bfloat16 rows) or, with an explicit kernel,
+    ``softmax_topk_ex``.  Another ``algo`` (see ``TOPK_ALGOS``) goes through
+    ``softmax_topk_algo``; the unfused ones write the softmax into ``y``
+    (allocated here when not given)."""
+    N, V = _batch(x)
+    vals, idx = _topk_outputs(x, N, K, vals, idx)
+    a = _algo(algo)
+    dt = _DTYPES[x.dtype]
+    if a != TOPK_ONLINE_FUSED:
+        if a in UNFUSED:
+            if y is None:
+                y = torch.empty_like(x)
+            elif (_batch(y, "y") != (N, V) or y.dtype != x.dtype or y.device != x.device):
+                raise ValueError("y must match x in shape, dtype and device")
+        yp = y.data_ptr() if (a in UNFUSED) else None
+        rc = lib().softmax_topk_algo(x.data_ptr(), yp, vals.data_ptr(), idx.data_ptr(), N, V,
+                                     int(K), dt, a, int(kernel), int(param), _stream(stream))
+    elif kernel != KERNEL_AUTO:
         rc = lib().softmax_topk_ex(x.data_ptr(), vals.data_ptr(), idx.data_ptr(), N, V,
-                                   int(K), _DTYPES[x.dtype], int(kernel), int(param),
-                                   _stream(stream))
+                                   int(K), dt, int(kernel), int(param), _stream(stream))
     elif x.dtype == torch.float32:
         rc = lib().softmax_topk(x.data_ptr(), vals.data_ptr(), idx.data_ptr(), N, V, int(K),
                                 _stream(stream))
     else:
         rc = lib().softmax_topk_dt(x.data_ptr(), vals.data_ptr(), idx.data_ptr(), N, V,
-                                   int(K), _DTYPES[x.dtype], _stream(stream))
+                                   int(K), dt, _stream(stream))
     if rc != OK:
         raise OsmError(rc, "softmax_topk")
     return vals, idx
 
 
 softmax_topk_dt = softmax_topk
+
+
+def topk(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,
+         idx: torch.Tensor | None = None, stream=None):
+    """(vals, idx) = the K largest elements of each row and their indices
+    (``topk_fwd``); larger first, equal values in increasing index order."""
+    N, V = _batch(x)
+    vals, idx = _topk_outputs(x, N, K, vals, idx)
+    rc = lib().topk_fwd(x.data_ptr(), vals.data_ptr(), idx.data_ptr(), N, V, int(K),
+                        _DTYPES[x.dtype], _stream(stream))
+    if rc != OK:
+        raise OsmError(rc, "topk_fwd")
+    return vals, idx
+
+
+def topk_plan(N: int, V: int, K: int, dtype=torch.float32):
+    """(kernel, param) that the top-k entry points use for this shape."""
+    k = ctypes.c_int()
+    p = ctypes.c_int64()
+    dt = _DTYPES[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    rc = lib().osm_topk_plan(int(N), int(V), dt, int(K), ctypes.byref(k), ctypes.byref(p))
+    if rc != OK:
+        raise OsmError(rc, "osm_topk_plan")
+    return k.value, p.value
 
 
 def plan(N: int, V: int, dtype=torch.float32, mode="online"):

@@ -153,29 +153,114 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
     return hip_status(f);
 }
 
-// Top-k shape: one wavefront per row once the batch alone can give every
-// SIMD several wavefronts; otherwise a workgroup (four wavefronts) per row.
-int64_t topk_lanes(int64_t N, int cus) { return N >= 4 * (int64_t)cus ? 64 : 256; }
+// Top-k plan: one wavefront per row once the batch alone can give every
+// SIMD several wavefronts; a small batch of long rows is split into chunks
+// (a workgroup each, about four workgroups per CU in all); otherwise a
+// workgroup (four wavefronts) per row.
+Plan choose_topk(int64_t N, int64_t V, int cus) {
+    if (N >= 4 * (int64_t)cus) return {OSM_KERNEL_ROWS, 64};
+    if (N < 2 * (int64_t)cus && V >= 16384) {
+        int64_t S = (4 * (int64_t)cus + N - 1) / N;
+        int64_t s_cap = V / 8192;  // keep chunks >= 8192 elements
+        if (S > s_cap) S = s_cap;
+        if (S >= 2) return {OSM_KERNEL_SPLIT, S};
+    }
+    return {OSM_KERNEL_ROWS, 256};
+}
 
-int run_topk(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K, int dtype,
-             int kernel, int64_t param, hipStream_t stream) {
+// One top-k pass of variant `var` over x (already validated).
+int launch_topk_pass(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
+                     int dtype, int var, int kernel, int64_t param, DeviceState* ds,
+                     hipStream_t stream) {
+    Plan p = kernel == OSM_KERNEL_AUTO ? choose_topk(N, V, ds->cus) : Plan{kernel, param};
+    osm::TopkLaunch a{x, vals, idx, nullptr, N, V, K, 1, 1, V, stream};
+    if (p.kernel == OSM_KERNEL_ROWS) {
+        a.waves_per_row = (int)(p.param / 64);
+        return hip_status(osm::launch_topk(a, dtype, var));
+    }
+    // split: chunk = ceil(V / S) rounded up to whole 16-byte vectors
+    const int64_t E = elems_per_vec(dtype);
+    int64_t S = p.param;
+    if (S > V) S = V;
+    int64_t chunk = (V + S - 1) / S;
+    chunk = (chunk + E - 1) / E * E;
+    S = (V + chunk - 1) / chunk;  // drop chunks that would start past the row
+    if (N * S > kMaxDim) return OSM_EINVAL;
+    if (S == 1) {  // one chunk is the whole row
+        a.waves_per_row = 4;
+        return hip_status(osm::launch_topk(a, dtype, var));
+    }
+    if (!ds->pool_ok) return OSM_ENOMEM;
+    void* scratch = nullptr;
+    if (hipMallocFromPoolAsync(&scratch, osm::topk_part_bytes(N, S, K), ds->pool, stream) !=
+            hipSuccess ||
+        !scratch) {
+        (void)hipGetLastError();
+        return OSM_ENOMEM;
+    }
+    a.part = scratch;
+    a.S = S;
+    a.chunk = chunk;
+    hipError_t e = osm::launch_topk(a, dtype, var);
+    hipError_t f = hipFreeAsync(scratch, stream);
+    if (e != hipSuccess) return OSM_EHIP;
+    return hip_status(f);
+}
+
+bool topk_algo_ok(int algo) {
+    return algo == OSM_TOPK_ONLINE_FUSED || algo == OSM_TOPK_SAFE_FUSED ||
+           algo == OSM_TOPK_SAFE_UNFUSED || algo == OSM_TOPK_ONLINE_UNFUSED ||
+           algo == OSM_TOPK_VALUES;
+}
+
+int run_topk(const void* x, void* y, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
+             int dtype, int algo, int kernel, int64_t param, hipStream_t stream) {
     size_t bytes = 0;
     if (!check_shape(N, V, dtype, &bytes)) return OSM_EINVAL;
     if (K < 1 || K > OSM_TOPK_KMAX || (int64_t)K > V) return OSM_EINVAL;
-    if (kernel != OSM_KERNEL_AUTO &&
-        !(kernel == OSM_KERNEL_ROWS && (param == 64 || param == 128 || param == 256)))
+    if (!topk_algo_ok(algo)) return OSM_EINVAL;
+    const bool unfused = algo == OSM_TOPK_SAFE_UNFUSED || algo == OSM_TOPK_ONLINE_UNFUSED;
+    if (kernel == OSM_KERNEL_ROWS) {
+        // the two-wavefront shape exists for the one-pass variant only
+        const bool two_ok = algo == OSM_TOPK_ONLINE_FUSED;
+        if (!(param == 64 || (param == 128 && two_ok) || param == 256)) return OSM_EINVAL;
+    } else if (kernel == OSM_KERNEL_SPLIT) {
+        if (param < 1 || param > kMaxDim || N * (param < V ? param : V) > kMaxDim)
+            return OSM_EINVAL;
+    } else if (kernel != OSM_KERNEL_AUTO) {
         return OSM_EINVAL;
+    }
     if (N == 0) return OSM_OK;
-    if (!x || !vals || !idx) return OSM_EINVAL;
-    if (!aligned(x, elem_size(dtype)) || !aligned(vals, 4) || !aligned(idx, 4)) return OSM_EINVAL;
+    if (!x || !vals || !idx || (unfused && !y)) return OSM_EINVAL;
+    const size_t es = elem_size(dtype);
+    if (!aligned(x, es) || !aligned(vals, 4) || !aligned(idx, 4)) return OSM_EINVAL;
     const size_t ob = (size_t)N * (size_t)K * 4;
     if (overlaps(x, bytes, vals, ob) || overlaps(x, bytes, idx, ob) || overlaps(vals, ob, idx, ob))
         return OSM_EINVAL;
+    if (unfused && (!aligned(y, es) || overlaps(y, bytes, x, bytes) ||
+                    overlaps(y, bytes, vals, ob) || overlaps(y, bytes, idx, ob)))
+        return OSM_EINVAL;
     DeviceState* ds = device_state(nullptr);
     if (!ds) return OSM_EHIP;
-    const int64_t lanes = kernel == OSM_KERNEL_AUTO ? topk_lanes(N, ds->cus) : param;
-    return hip_status(
-        osm::launch_topk_fused(x, vals, idx, N, V, K, dtype, (int)(lanes / 64), stream));
+    switch (algo) {
+        case OSM_TOPK_ONLINE_FUSED:
+            return launch_topk_pass(x, vals, idx, N, V, K, dtype, osm::TK_ONLINE, kernel, param,
+                                    ds, stream);
+        case OSM_TOPK_SAFE_FUSED:
+            return launch_topk_pass(x, vals, idx, N, V, K, dtype, osm::TK_SAFE, kernel, param, ds,
+                                    stream);
+        case OSM_TOPK_VALUES:
+            return launch_topk_pass(x, vals, idx, N, V, K, dtype, osm::TK_VALUES, kernel, param,
+                                    ds, stream);
+        default: {
+            // softmax into y (Alg. 2 or Alg. 3), then a separate top-k over y
+            const int mode = algo == OSM_TOPK_SAFE_UNFUSED ? OSM_SAFE : OSM_ONLINE;
+            int st = run_softmax(x, y, N, V, dtype, mode, OSM_KERNEL_AUTO, 0, stream);
+            if (st != OSM_OK) return st;
+            return launch_topk_pass(y, vals, idx, N, V, K, dtype, osm::TK_VALUES, kernel, param,
+                                    ds, stream);
+        }
+    }
 }
 
 }  // namespace
@@ -194,17 +279,43 @@ int softmax_fwd_ex(const void* x, void* y, int64_t N, int64_t V, int dtype, int 
 
 int softmax_topk(const float* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
                  hipStream_t stream) {
-    return run_topk(x, vals, idx, N, V, K, OSM_F32, OSM_KERNEL_AUTO, 0, stream);
+    return run_topk(x, nullptr, vals, idx, N, V, K, OSM_F32, OSM_TOPK_ONLINE_FUSED,
+                    OSM_KERNEL_AUTO, 0, stream);
 }
 
 int softmax_topk_dt(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
                     int dtype, hipStream_t stream) {
-    return run_topk(x, vals, idx, N, V, K, dtype, OSM_KERNEL_AUTO, 0, stream);
+    return run_topk(x, nullptr, vals, idx, N, V, K, dtype, OSM_TOPK_ONLINE_FUSED,
+                    OSM_KERNEL_AUTO, 0, stream);
 }
 
 int softmax_topk_ex(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
                     int dtype, int kernel, int64_t param, hipStream_t stream) {
-    return run_topk(x, vals, idx, N, V, K, dtype, kernel, param, stream);
+    return run_topk(x, nullptr, vals, idx, N, V, K, dtype, OSM_TOPK_ONLINE_FUSED, kernel, param,
+                    stream);
+}
+
+int softmax_topk_algo(const void* x, void* y, float* vals, int32_t* idx, int64_t N, int64_t V,
+                      int K, int dtype, int algo, int kernel, int64_t param, hipStream_t stream) {
+    return run_topk(x, y, vals, idx, N, V, K, dtype, algo, kernel, param, stream);
+}
+
+int topk_fwd(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K, int dtype,
+             hipStream_t stream) {
+    return run_topk(x, nullptr, vals, idx, N, V, K, dtype, OSM_TOPK_VALUES, OSM_KERNEL_AUTO, 0,
+                    stream);
+}
+
+int osm_topk_plan(int64_t N, int64_t V, int dtype, int K, int* kernel, int64_t* param) {
+    size_t bytes = 0;
+    if (!check_shape(N, V, dtype, &bytes)) return OSM_EINVAL;
+    if (K < 1 || K > OSM_TOPK_KMAX || (int64_t)K > V) return OSM_EINVAL;
+    if (!kernel || !param) return OSM_EINVAL;
+    DeviceState* ds = device_state(nullptr);
+    Plan p = choose_topk(N, V, ds ? ds->cus : 256);
+    *kernel = p.kernel;
+    *param = p.param;
+    return OSM_OK;
 }
 
 int osm_plan(int64_t N, int64_t V, int dtype, int mode, int* kernel, int64_t* param) {

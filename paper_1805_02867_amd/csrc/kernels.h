@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace osm {
@@ -17,9 +18,48 @@ hipError_t launch_softmax_split(const void* x, void* y, void* scratch, int64_t N
                                 int dtype, int mode, int64_t S, int64_t chunk, bool vec,
                                 hipStream_t st);
 
-// Fused online softmax + top-k; waves_per_row = 1 (four rows per workgroup)
-// or 4 (one row per workgroup).
-hipError_t launch_topk_fused(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V,
-                             int K, int dtype, int waves_per_row, hipStream_t st);
+// What the top-k kernels compute next to the selection (Section 4, and the
+// comparisons of Section 5.2):
+//  TK_ONLINE: the online pair, one pass (Alg. 4);
+//  TK_SAFE:   a maximum pass over the row first, then the normalizer with
+//             that maximum held fixed, in the pass that selects (the safe
+//             softmax fused with top-k: two loads per element);
+//  TK_VALUES: no softmax; the outputs are the selected inputs themselves
+//             (the separate top-k of the unfused comparisons).
+enum TopkVar { TK_ONLINE = 0, TK_SAFE = 1, TK_VALUES = 2 };
+
+struct TopkLaunch {
+    const void* x;
+    float* vals;
+    int32_t* idx;
+    void* part;          // split scratch (S > 1): topk_part_bytes(N, S, K) bytes
+    int64_t N, V;
+    int K;
+    int waves_per_row;   // S <= 1: 1, 2 (TK_ONLINE only) or 4
+    int64_t S, chunk;    // chunks per row and their length in elements (S > 1)
+    hipStream_t st;
+};
+
+// Split scratch: N * S * K 64-bit keys, then N * S normalizer pairs.
+inline size_t topk_part_bytes(int64_t N, int64_t S, int64_t K) {
+    return (size_t)N * (size_t)S * ((size_t)K * 8 + 8);
+}
+
+hipError_t launch_topk_online_f32(const TopkLaunch& a);
+hipError_t launch_topk_online_bf16(const TopkLaunch& a);
+hipError_t launch_topk_safe_f32(const TopkLaunch& a);
+hipError_t launch_topk_safe_bf16(const TopkLaunch& a);
+hipError_t launch_topk_values_f32(const TopkLaunch& a);
+hipError_t launch_topk_values_bf16(const TopkLaunch& a);
+
+inline hipError_t launch_topk(const TopkLaunch& a, int dtype, int var) {
+    const bool bf = dtype == 1;
+    switch (var) {
+        case TK_ONLINE: return bf ? launch_topk_online_bf16(a) : launch_topk_online_f32(a);
+        case TK_SAFE: return bf ? launch_topk_safe_bf16(a) : launch_topk_safe_f32(a);
+        case TK_VALUES: return bf ? launch_topk_values_bf16(a) : launch_topk_values_f32(a);
+        default: return hipErrorInvalidValue;
+    }
+}
 
 }  // namespace osm

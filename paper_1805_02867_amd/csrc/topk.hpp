@@ -43,6 +43,10 @@
 // fill the chip when the batch is small.  Each step issues all of a lane's loads
 // before processing any, so a wavefront keeps U KiB in flight; loads carry
 // non-temporal hints since every element is read exactly once.
+#pragma once
+
+#include <type_traits>
+
 #include "md.hpp"
 #include "kernels.h"
 
@@ -350,13 +354,30 @@ __device__ __forceinline__ void widen(u32x4 q, float (&x)[Vec<T>::N]) {
     }
 }
 
-// W wavefronts per row; TK_BLOCK / (64 W) rows per workgroup; U 16-byte
-// vectors per lane per step, all loaded before any is processed.
-template <typename T, int W, int U>
+// d += sum_i 2^{x_i log2e - s} with s held fixed (the safe normalizer).
+template <int N>
+__device__ __forceinline__ float sum_exp_fixed(float d, const float (&x)[N], float s) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) d += exp2_hw(__builtin_fmaf(x[i], kLog2e, -s));
+    return d;
+}
+
+// W wavefronts per (virtual) row; TK_BLOCK / (64 W) of them per workgroup;
+// U 16-byte vectors per lane per step.
+//
+// Virtual rows.  Row r of the batch is cut into `segs` chunks of `seg`
+// elements (the last one shorter); virtual row v = r * segs + c covers chunk
+// c.  With segs = 1 a virtual row is a row.  PART = false writes the final
+// outputs (segs must be 1); PART = true writes, per virtual row, its K
+// largest keys (indices relative to the start of the row; 0 = fewer than K)
+// and its normalizer pair, which topk_merge combines.
+template <typename T, int W, int U, int VAR, bool PART>
 __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
                                                       float* __restrict__ vals,
-                                                      int32_t* __restrict__ idx, int64_t N,
-                                                      int64_t V, int K) {
+                                                      int32_t* __restrict__ idx,
+                                                      uint64_t* __restrict__ pkeys,
+                                                      MD* __restrict__ pmd, int64_t N, int64_t V,
+                                                      int K, int64_t seg, int64_t segs) {
     constexpr int E = Vec<T>::N;
     constexpr int WB = TK_BLOCK / 64;       // wavefronts per workgroup
     constexpr int RB = WB / W;              // rows per workgroup
@@ -365,51 +386,34 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     __shared__ uint64_t region[WB][TK_REGION];
     __shared__ uint64_t published[WB];
     __shared__ MD wmd[WB];
+    __shared__ float wmx[WB];
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int rw = wv % W;                  // wavefront within the row
     const int tr = tid % TR;                // thread within the row
-    const int64_t row = (int64_t)blockIdx.x * RB + wv / W;
-    const bool live = row < N;              // uniform per wavefront (and per row)
+    const int64_t vr = (int64_t)blockIdx.x * RB + wv / W;
+    const bool live = vr < N * segs;        // uniform per wavefront (and per row)
 
     if (lane < K) region[wv][lane] = 0;     // empty list
     if (lane == 0) published[wv] = 0;
     if constexpr (W > 1) __syncthreads();
     if (!live) return;                      // whole rows leave together
 
-    const T* xr = x + row * V;
+    const int64_t row = PART ? vr / segs : vr;
+    const int64_t start = PART ? (vr - row * segs) * seg : 0;
+    const int64_t L = PART ? (V - start < seg ? V - start : seg) : V;
+    const uint32_t base = (uint32_t)start;  // index of the chunk's first element
+    const T* xr = x + row * V + start;
     TopkWave<W> tw{region[wv], published + (wv / W) * W, rw, K, 0, 0ull, -__builtin_inff(),
                    0ull};
 
-    // split of the row into scalar head, 16-byte vectors, scalar tail
+    // split of the chunk into scalar head, 16-byte vectors, scalar tail
     int64_t head = ((16 - (int64_t)(((uintptr_t)xr) & 15)) & 15) / (int64_t)sizeof(T);
-    if (head > V) head = V;
-    const int64_t nvec = (V - head) / E;
+    if (head > L) head = L;
+    const int64_t nvec = (L - head) / E;
     const int64_t tail0 = head + nvec * E;
     const u32x4* vb = reinterpret_cast<const u32x4*>(xr + head);
 
-    MD st[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) st[u] = md_empty();
-
-    // scalar head and tail: wave-uniform loops, one element per lane
-    for (int64_t b0 = 0; b0 < head; b0 += TR) {
-        int64_t i = b0 + tr;
-        bool ok = i < head;
-        float v[1] = {ok ? load1(xr + i) : -__builtin_inff()};
-        if (ok) st[0] = md_fold1(st[0], v[0]);
-        tw.template offer<1>(v, (uint32_t)i, ok);
-    }
-    for (int64_t b0 = tail0; b0 < V; b0 += TR) {
-        int64_t i = b0 + tr;
-        bool ok = i < V;
-        float v[1] = {ok ? load1(xr + i) : -__builtin_inff()};
-        if (ok) st[0] = md_fold1(st[0], v[0]);
-        tw.template offer<1>(v, (uint32_t)i, ok);
-    }
-
-    // vector body: every lane runs the same number of steps so that the
-    // wavefront-wide queue operations see all 64 lanes
     const u32x4 ninf = (E == 4) ? u32x4{0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u}
                                 : u32x4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
     // Full steps (every lane holds U whole vectors) run as a software
@@ -421,13 +425,105 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     const int64_t nfull = nvec / STEP;
     const int fa = flush_at(K);
     const u32x4* lp = vb + tr;  // this lane's first vector
-    auto load_full = [&](u32x4 (&buf)[U], int64_t sidx) {
+    // NT: the last read of the data (non-temporal hint)
+    auto load_full = [&](u32x4 (&buf)[U], int64_t sidx, auto nt) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) buf[u] = __builtin_nontemporal_load(lp + sidx * STEP + u * TR);
+        for (int u = 0; u < U; ++u) {
+            if constexpr (decltype(nt)::value)
+                buf[u] = __builtin_nontemporal_load(lp + sidx * STEP + u * TR);
+            else
+                buf[u] = lp[sidx * STEP + u * TR];
+        }
         // keep the scheduler from hoisting the next step's work above these
         // loads (that would make it wait for the previous buffer first)
         __builtin_amdgcn_sched_barrier(0);
     };
+    auto lane_max_of = [&](const u32x4 (&buf)[U], const bool (&ok)[U], bool masked) {
+        float lm = -__builtin_inff();
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            float xv[E];
+            widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
+            lm = fmaxf(lm, vec_max(xv));
+        }
+        return lm;
+    };
+    bool all_ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) all_ok[u] = true;
+
+    MD st[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) st[u] = md_empty();
+
+    // Safe variant: the row's maximum first (plain loads, so that the second
+    // read may still find the data in cache), then s = max * log2e is held
+    // fixed: the pairs only sum.
+    float sfix = 0.0f;
+    if constexpr (VAR == TK_SAFE) {
+        float mx = -__builtin_inff();
+        for (int64_t i = tr; i < head; i += TR) mx = fmaxf(mx, load1(xr + i));
+        for (int64_t i = tail0 + tr; i < L; i += TR) mx = fmaxf(mx, load1(xr + i));
+        if (nfull > 0) {
+            u32x4 ba[U], bb[U];
+            load_full(ba, 0, std::false_type{});
+            int64_t j = 0;
+            for (; j + 2 <= nfull; j += 2) {
+                load_full(bb, j + 1, std::false_type{});
+                mx = fmaxf(mx, lane_max_of(ba, all_ok, false));
+                load_full(ba, (j + 2 < nfull) ? j + 2 : j + 1, std::false_type{});
+                mx = fmaxf(mx, lane_max_of(bb, all_ok, false));
+            }
+            if (j < nfull) mx = fmaxf(mx, lane_max_of(ba, all_ok, false));
+        }
+        if (nfull * STEP < nvec) {
+            const int64_t b0 = nfull * STEP, vlast = nvec - 1;
+            u32x4 bt[U];
+            bool ok[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t vi = b0 + (int64_t)u * TR + tr;
+                ok[u] = vi < nvec;
+                bt[u] = vb[vi < nvec ? vi : vlast];
+            }
+            mx = fmaxf(mx, lane_max_of(bt, ok, true));
+        }
+        mx = group_max<64>(mx);
+        if constexpr (W > 1) {
+            if (lane == 0) wmx[wv] = mx;
+            __syncthreads();
+            const int w0 = wv - rw;
+#pragma unroll
+            for (int w = 0; w < W; ++w) mx = fmaxf(mx, wmx[w0 + w]);
+        }
+        // a row of -inf keeps the empty reference (d stays 0); NaN and +inf
+        // reach d as NaN, as in the online pair
+        sfix = mx * kLog2e;
+        if (!(sfix > kEmptyS)) sfix = kEmptyS;
+#pragma unroll
+        for (int u = 0; u < U; ++u) st[u] = MD{sfix, 0.0f};
+    }
+    auto fold1 = [&](float v) {
+        if constexpr (VAR == TK_ONLINE) st[0] = md_fold1(st[0], v);
+        else if constexpr (VAR == TK_SAFE) st[0].d += exp2_hw(__builtin_fmaf(v, kLog2e, -sfix));
+    };
+
+    // scalar head and tail: wave-uniform loops, one element per lane
+    for (int64_t b0 = 0; b0 < head; b0 += TR) {
+        int64_t i = b0 + tr;
+        bool ok = i < head;
+        float v[1] = {ok ? load1(xr + i) : -__builtin_inff()};
+        if (ok) fold1(v[0]);
+        tw.template offer<1>(v, base + (uint32_t)i, ok);
+    }
+    for (int64_t b0 = tail0; b0 < L; b0 += TR) {
+        int64_t i = b0 + tr;
+        bool ok = i < L;
+        float v[1] = {ok ? load1(xr + i) : -__builtin_inff()};
+        if (ok) fold1(v[0]);
+        tw.template offer<1>(v, base + (uint32_t)i, ok);
+    }
+
     // Bootstrap: the K-th largest distinct value among the lanes' maxima
     // over the first step bounds the row's K-th value from below; keys
     // >= (that value, any index) are kept, i.e. keys > (value key with index
@@ -465,7 +561,8 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
             widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
             mxs[u] = vec_max(xv);
             lane_mx = fmaxf(lane_mx, mxs[u]);
-            st[u] = md_fold_lazy(st[u], xv, mxs[u]);
+            if constexpr (VAR == TK_ONLINE) st[u] = md_fold_lazy(st[u], xv, mxs[u]);
+            else if constexpr (VAR == TK_SAFE) st[u].d = sum_exp_fixed(st[u].d, xv, sfix);
         }
         if (__builtin_amdgcn_ballot_w64(lane_mx >= tw.tau_v) != 0) {
 #pragma unroll
@@ -474,39 +571,26 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
                     float xv[E];
                     widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
                     const int64_t e0 = head + (b0 + (int64_t)u * TR + tr) * E;
-                    tw.template offer<E>(xv, (uint32_t)e0, ok[u]);
+                    tw.template offer<E>(xv, base + (uint32_t)e0, ok[u]);
                 }
             }
         }
         if (tw.qcount >= fa) tw.flush();
         tw.pull();
     };
-    auto lane_max_of = [&](const u32x4 (&buf)[U], const bool (&ok)[U], bool masked) {
-        float lm = -__builtin_inff();
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            float xv[E];
-            widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
-            lm = fmaxf(lm, vec_max(xv));
-        }
-        return lm;
-    };
 
-    bool all_ok[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) all_ok[u] = true;
     bool booted = false;
     if (nfull > 0) {
         u32x4 ba[U], bb[U];
-        load_full(ba, 0);
+        load_full(ba, 0, std::true_type{});
         const float lm[1] = {lane_max_of(ba, all_ok, false)};
         bootstrap(lm);
         booted = true;
         int64_t j = 0;
         for (; j + 2 <= nfull; j += 2) {
-            load_full(bb, j + 1);
+            load_full(bb, j + 1, std::true_type{});
             step(ba, all_ok, j * STEP, false);
-            load_full(ba, (j + 2 < nfull) ? j + 2 : j + 1);  // stays inside the row
+            load_full(ba, (j + 2 < nfull) ? j + 2 : j + 1, std::true_type{});  // stays inside the row
             step(bb, all_ok, (j + 1) * STEP, false);
         }
         if (j < nfull) step(ba, all_ok, j * STEP, false);
@@ -533,9 +617,11 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     // merge of the normalizer pairs: wavefront butterflies, then (W > 1)
     // a fixed-order merge of the row's wavefronts
     MD md = st[0];
+    if constexpr (VAR != TK_VALUES) {
 #pragma unroll
-    for (int u = 1; u < U; ++u) md = md_merge(md, st[u]);
-    md = group_merge<64>(md);
+        for (int u = 1; u < U; ++u) md = md_merge(md, st[u]);
+        md = group_merge<64>(md);
+    }
     uint64_t key = tw.mine;
     if constexpr (W > 1) {
         if (lane == 0) wmd[wv] = md;
@@ -551,9 +637,69 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
         int found;
         key = select_topk<W>(e, W, K, &found);
     }
+    if constexpr (PART) {
+        if (lane < K) pkeys[vr * K + lane] = key;
+        if (VAR != TK_VALUES && lane == 0) pmd[vr] = md;
+    } else if (lane < K) {
+        if constexpr (VAR == TK_VALUES) {
+            vals[row * K + lane] = key_value(key);
+        } else {
+            const float S = md.s, rd = 1.0f / md.d;
+            vals[row * K + lane] = exp2_hw(__builtin_fmaf(key_value(key), kLog2e, -S)) * rd;
+        }
+        idx[row * K + lane] = key_index(key);
+    }
+}
+
+// Second stage of the split top-k: per row, the K largest of the S * K
+// chunk keys (filtered against the running threshold as in the one-pass
+// kernel) and the fixed-order merge (Eq. 4) of the S chunk pairs.  One
+// wavefront per row.
+constexpr int TK_MERGE_B = 8;  // keys per lane in flight
+
+template <int VAR>
+__global__ __launch_bounds__(TK_BLOCK) void topk_merge(const uint64_t* __restrict__ pkeys,
+                                                      const MD* __restrict__ pmd,
+                                                      float* __restrict__ vals,
+                                                      int32_t* __restrict__ idx, int64_t N,
+                                                      int64_t S, int K) {
+    constexpr int WB = TK_BLOCK / 64;
+    __shared__ uint64_t region[WB][TK_REGION];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int64_t row = (int64_t)blockIdx.x * WB + wv;
+    if (lane < K) region[wv][lane] = 0;
+    if (row >= N) return;
+    TopkWave<1> tw{region[wv], nullptr, 0, K, 0, 0ull, -__builtin_inff(), 0ull};
+    const int fa = flush_at(K);
+    const int64_t n = S * K;
+    const uint64_t* pk = pkeys + row * n;
+    for (int64_t c = 0; c < n; c += 64 * TK_MERGE_B) {
+        uint64_t k[TK_MERGE_B];
+#pragma unroll
+        for (int b = 0; b < TK_MERGE_B; ++b) {
+            const int64_t j = c + b * 64 + lane;
+            k[b] = j < n ? pk[j] : 0ull;
+        }
+#pragma unroll
+        for (int b = 0; b < TK_MERGE_B; ++b) {
+            tw.append(k[b] > tw.tau, k[b]);  // 0 (absent) never passes
+            if (tw.qcount >= fa) tw.flush();
+        }
+    }
+    tw.flush();
+    const uint64_t key = tw.mine;
+    MD md = md_empty();
+    if constexpr (VAR != TK_VALUES) {
+        for (int64_t j = lane; j < S; j += 64) md = md_merge(md, pmd[row * S + j]);
+        md = group_merge<64>(md);  // every lane takes part
+    }
     if (lane < K) {
-        const float S = md.s, rd = 1.0f / md.d;
-        vals[row * K + lane] = exp2_hw(__builtin_fmaf(key_value(key), kLog2e, -S)) * rd;
+        if constexpr (VAR == TK_VALUES) {
+            vals[row * K + lane] = key_value(key);
+        } else {
+            const float Sv = md.s, rd = 1.0f / md.d;
+            vals[row * K + lane] = exp2_hw(__builtin_fmaf(key_value(key), kLog2e, -Sv)) * rd;
+        }
         idx[row * K + lane] = key_index(key);
     }
 }
@@ -574,39 +720,57 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
 #define OSM_TOPK_U4 2
 #endif
 
-hipError_t launch_topk_fused(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V,
-                             int K, int dtype, int waves_per_row, hipStream_t st) {
-    if (K < 1 || K > TK_KMAX) return hipErrorInvalidValue;
+template <typename T, int W>
+constexpr int topk_unroll() {
+    if constexpr (W == 1) return std::is_same<T, float>::value ? OSM_TOPK_U1 : OSM_TOPK_U1B;
+    else if constexpr (W == 2) return std::is_same<T, float>::value ? OSM_TOPK_U2 : OSM_TOPK_U1B;
+    else return OSM_TOPK_U4;
+}
+
+// Launch of one variant for one element type (see TopkLaunch).
+template <typename T, int VAR>
+hipError_t launch_topk_t(const TopkLaunch& a) {
     dim3 block(TK_BLOCK);
-    if (waves_per_row == 1) {
-        constexpr int RB = TK_BLOCK / 64;
-        dim3 grid((unsigned)((N + RB - 1) / RB));
-        if (dtype == 0)
-            hipLaunchKernelGGL((topk_fused<float, 1, OSM_TOPK_U1>), grid, block, 0, st, (const float*)x, vals,
-                               idx, N, V, K);
-        else
-            hipLaunchKernelGGL((topk_fused<bf16_t, 1, OSM_TOPK_U1B>), grid, block, 0, st, (const bf16_t*)x,
-                               vals, idx, N, V, K);
-    } else if (waves_per_row == 2) {
-        constexpr int RB = TK_BLOCK / 128;
-        dim3 grid((unsigned)((N + RB - 1) / RB));
-        if (dtype == 0)
-            hipLaunchKernelGGL((topk_fused<float, 2, OSM_TOPK_U2>), grid, block, 0, st,
-                               (const float*)x, vals, idx, N, V, K);
-        else
-            hipLaunchKernelGGL((topk_fused<bf16_t, 2, OSM_TOPK_U1B>), grid, block, 0, st,
-                               (const bf16_t*)x, vals, idx, N, V, K);
-    } else if (waves_per_row == 4) {
-        dim3 grid((unsigned)N);
-        if (dtype == 0)
-            hipLaunchKernelGGL((topk_fused<float, 4, OSM_TOPK_U4>), grid, block, 0, st, (const float*)x, vals,
-                               idx, N, V, K);
-        else
-            hipLaunchKernelGGL((topk_fused<bf16_t, 4, OSM_TOPK_U4>), grid, block, 0, st, (const bf16_t*)x,
-                               vals, idx, N, V, K);
-    } else {
-        return hipErrorInvalidValue;
+    const T* x = static_cast<const T*>(a.x);
+    if (a.S <= 1) {
+        if (a.waves_per_row == 1) {
+            constexpr int RB = TK_BLOCK / 64;
+            dim3 grid((unsigned)((a.N + RB - 1) / RB));
+            hipLaunchKernelGGL((topk_fused<T, 1, topk_unroll<T, 1>(), VAR, false>), grid, block, 0,
+                               a.st, x, a.vals, a.idx, nullptr, nullptr, a.N, a.V, a.K, a.V,
+                               (int64_t)1);
+        } else if (a.waves_per_row == 2) {
+            if constexpr (VAR == TK_ONLINE) {  // the two-wavefront shape is built for Alg. 4 only
+                constexpr int RB = TK_BLOCK / 128;
+                dim3 grid((unsigned)((a.N + RB - 1) / RB));
+                hipLaunchKernelGGL((topk_fused<T, 2, topk_unroll<T, 2>(), VAR, false>), grid,
+                                   block, 0, a.st, x, a.vals, a.idx, nullptr, nullptr, a.N, a.V,
+                                   a.K, a.V, (int64_t)1);
+            } else {
+                return hipErrorInvalidValue;
+            }
+        } else if (a.waves_per_row == 4) {
+            dim3 grid((unsigned)a.N);
+            hipLaunchKernelGGL((topk_fused<T, 4, topk_unroll<T, 4>(), VAR, false>), grid, block, 0,
+                               a.st, x, a.vals, a.idx, nullptr, nullptr, a.N, a.V, a.K, a.V,
+                               (int64_t)1);
+        } else {
+            return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
     }
+    // split: chunks of a.chunk elements, one workgroup (four wavefronts) each
+    uint64_t* pkeys = static_cast<uint64_t*>(a.part);
+    MD* pmd = reinterpret_cast<MD*>(pkeys + a.N * a.S * a.K);
+    dim3 grid((unsigned)(a.N * a.S));
+    hipLaunchKernelGGL((topk_fused<T, 4, topk_unroll<T, 4>(), VAR, true>), grid, block, 0, a.st,
+                       x, nullptr, nullptr, pkeys, pmd, a.N, a.V, a.K, a.chunk, a.S);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    constexpr int WB = TK_BLOCK / 64;
+    dim3 mgrid((unsigned)((a.N + WB - 1) / WB));
+    hipLaunchKernelGGL((topk_merge<VAR>), mgrid, block, 0, a.st, pkeys, pmd, a.vals, a.idx, a.N,
+                       a.S, a.K);
     return hipGetLastError();
 }
 

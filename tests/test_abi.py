@@ -22,7 +22,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("softmax_fwd", "softmax_fwd_ex", "softmax_topk", "softmax_topk_dt",
-                 "softmax_topk_ex", "osm_plan", "osm_status_string"):
+                 "softmax_topk_ex", "softmax_topk_algo", "topk_fwd", "osm_plan",
+                 "osm_topk_plan", "osm_status_string"):
         assert want in names
 
 
@@ -38,7 +39,12 @@ def test_enum_values_match_header():
                       ("OSM_SAFE", osm.SAFE), ("OSM_ONLINE", osm.ONLINE), ("OSM_OK", osm.OK),
                       ("OSM_EINVAL", osm.EINVAL), ("OSM_EHIP", osm.EHIP),
                       ("OSM_ENOMEM", osm.ENOMEM), ("OSM_KERNEL_ROWS", osm.KERNEL_ROWS),
-                      ("OSM_KERNEL_SPLIT", osm.KERNEL_SPLIT)):
+                      ("OSM_KERNEL_SPLIT", osm.KERNEL_SPLIT),
+                      ("OSM_TOPK_ONLINE_FUSED", osm.TOPK_ONLINE_FUSED),
+                      ("OSM_TOPK_SAFE_FUSED", osm.TOPK_SAFE_FUSED),
+                      ("OSM_TOPK_SAFE_UNFUSED", osm.TOPK_SAFE_UNFUSED),
+                      ("OSM_TOPK_ONLINE_UNFUSED", osm.TOPK_ONLINE_UNFUSED),
+                      ("OSM_TOPK_VALUES", osm.TOPK_VALUES)):
         assert re.search(rf"\b{name}\s*=\s*{val}\b", text), name
     assert re.search(rf"#define OSM_TOPK_KMAX {osm.TOPK_KMAX}\b", text)
 
@@ -99,9 +105,41 @@ def test_softmax_topk_rejects(args):
     assert osm.lib().softmax_topk(*args, None) == osm.EINVAL
 
 
-@pytest.mark.parametrize("kernel,param", [(2, 4), (1, 32), (1, 512), (1, 0), (5, 64)])
+@pytest.mark.parametrize("kernel,param", [(2, 0), (2, -3), (2, 1 << 31), (1, 32), (1, 512),
+                                          (1, 0), (5, 64)])
 def test_softmax_topk_ex_rejects(kernel, param):
     assert osm.lib().softmax_topk_ex(X, V_, I_, 4, 10, 5, 0, kernel, param, None) == osm.EINVAL
+
+
+Y_ = 0x50000000
+
+
+@pytest.mark.parametrize("args", [
+    (X, Y_, V_, I_, 4, 10, 5, 0, 5, 0, 0),     # unknown algo
+    (X, Y_, V_, I_, 4, 10, 5, 0, -1, 0, 0),    # unknown algo
+    (X, 0, V_, I_, 4, 10, 5, 0, 2, 0, 0),      # safe unfused without y
+    (X, 0, V_, I_, 4, 10, 5, 0, 3, 0, 0),      # online unfused without y
+    (X, X + 8, V_, I_, 4, 10, 5, 0, 2, 0, 0),  # y overlaps x
+    (X, V_, V_, I_, 4, 10, 5, 0, 3, 0, 0),     # y overlaps vals
+    (X, Y_ + 2, V_, I_, 4, 10, 5, 0, 2, 0, 0), # y misaligned
+    (X, 0, V_, I_, 4, 10, 5, 0, 1, 1, 128),    # two-wavefront shape: Alg. 4 only
+    (X, 0, V_, I_, 4, 10, 5, 0, 4, 1, 128),
+    (X, 0, V_, I_, 4, 10, 5, 0, 1, 2, 0),      # split with no chunk
+    (X, 0, V_, I_, 4, 10, 11, 0, 1, 0, 0),     # K > V
+])
+def test_softmax_topk_algo_rejects(args):
+    assert osm.lib().softmax_topk_algo(*args, None) == osm.EINVAL
+
+
+@pytest.mark.parametrize("args", [
+    (X, V_, I_, 4, 10, 11, 0),     # K > V
+    (X, V_, I_, 4, 10, 0, 0),      # K < 1
+    (0, V_, I_, 4, 10, 5, 0),      # null x
+    (X, V_, I_, 4, 10, 5, 3),      # unknown dtype
+    (X, X + 4, I_, 4, 10, 5, 0),   # vals overlaps x
+])
+def test_topk_fwd_rejects(args):
+    assert osm.lib().topk_fwd(*args, None) == osm.EINVAL
 
 
 def test_softmax_topk_dt_rejects_unknown_dtype():
@@ -117,9 +155,20 @@ def test_plan_rejects_bad_shapes():
     assert osm.lib().osm_plan(4, 10, 0, 2, None, ctypes.byref(p)) == osm.EINVAL
 
 
+def test_topk_plan_rejects_bad_arguments():
+    k = ctypes.c_int()
+    p = ctypes.c_int64()
+    assert osm.lib().osm_topk_plan(4, 0, 0, 5, ctypes.byref(k), ctypes.byref(p)) == osm.EINVAL
+    assert osm.lib().osm_topk_plan(4, 10, 0, 11, ctypes.byref(k), ctypes.byref(p)) == osm.EINVAL
+    assert osm.lib().osm_topk_plan(4, 100, 0, 65, ctypes.byref(k), ctypes.byref(p)) == osm.EINVAL
+    assert osm.lib().osm_topk_plan(4, 10, 0, 5, None, ctypes.byref(p)) == osm.EINVAL
+
+
 def test_python_binding_refuses_cpu_tensors():
     import torch
     with pytest.raises(ValueError):
         osm.softmax_fwd(torch.zeros(2, 3))
     with pytest.raises(ValueError):
         osm.softmax_topk(torch.zeros(2, 3), 1)
+    with pytest.raises(ValueError):
+        osm.topk(torch.zeros(2, 3), 1)

@@ -151,7 +151,7 @@ def test_workload_32768x128256_bf16_k50_sampled(dev):
     torch.cuda.synchronize()
     g = torch.Generator().manual_seed(321)
     rows = torch.cat([torch.tensor([0, w["N"] - 1]),
-                      torch.randperm(w["N"], generator=g)[:1024]])
+                      torch.randperm(w["N"], generator=g)[:4096]])
     rr = rows.to(dev)
     xh = to_host(x.index_select(0, rr))
     v64, z64 = oracle.topk(xh, w["K"], "bf16")
