@@ -28,8 +28,12 @@
  *    below 2.35e38 (x * log2(e) must be finite).  Top-k of a NaN row is
  *    unspecified.
  *  - Thread safety: calls may be made concurrently from several host threads
- *    and streams.  The only shared state is a per-device cache of device
- *    properties and a per-device stream-ordered memory pool.
+ *    and streams.  The shared state is a per-device cache of device
+ *    properties, a per-device stream-ordered memory pool, and the scratch of
+ *    the split kernels, kept per stream (up to 64 streams per device; a
+ *    buffer grows in stream order and is kept until the process ends; work
+ *    of a destroyed stream must have finished before a new stream with the
+ *    same handle calls the library).
  */
 #ifndef OSOFTMAX_H
 #define OSOFTMAX_H

@@ -17,11 +17,25 @@ size_t elem_size(int dtype) { return dtype == OSM_BF16 ? 2 : 4; }
 int elems_per_vec(int dtype) { return dtype == OSM_BF16 ? 8 : 4; }
 
 // ------------------------------------------------------------ device state
+// Scratch of the split kernels, cached per stream: work on one stream runs in
+// order, so successive calls on a stream share a buffer without allocating;
+// distinct streams get distinct buffers.
+struct ScratchSlot {
+    hipStream_t stream;
+    void* ptr;
+    size_t bytes;
+};
+constexpr int kScratchSlots = 64;
+constexpr size_t kScratchMin = 256 * 1024;
+
 struct DeviceState {
     std::once_flag once;
     int cus = 0;
     hipMemPool_t pool = nullptr;
     bool pool_ok = false;
+    std::mutex mu;  // guards the scratch table
+    ScratchSlot slots[kScratchSlots] = {};
+    int nslots = 0;
 };
 DeviceState g_dev[kMaxDevices];
 
@@ -52,6 +66,45 @@ DeviceState* device_state(int* dev_out) {
     });
     if (dev_out) *dev_out = dev;
     return &s;
+}
+
+// Scratch of at least `bytes` for work enqueued on `stream`.  A stream's
+// buffer grows by a stream-ordered allocation from the library pool (the old
+// one is freed in stream order behind the work already enqueued) and is kept
+// until the process ends.  Once the table is full, a call gets a buffer of
+// its own (*temp = true) that it frees in stream order after its launches.
+int acquire_scratch(DeviceState* ds, hipStream_t stream, size_t bytes, void** out, bool* temp) {
+    if (!ds->pool_ok) return OSM_ENOMEM;
+    std::lock_guard<std::mutex> guard(ds->mu);
+    ScratchSlot* slot = nullptr;
+    for (int i = 0; i < ds->nslots; ++i)
+        if (ds->slots[i].stream == stream) slot = &ds->slots[i];
+    if (!slot && ds->nslots < kScratchSlots) {
+        slot = &ds->slots[ds->nslots++];
+        *slot = ScratchSlot{stream, nullptr, 0};
+    }
+    *temp = slot == nullptr;
+    if (slot && slot->bytes >= bytes) {
+        *out = slot->ptr;
+        return OSM_OK;
+    }
+    size_t want = bytes;
+    if (slot) {
+        want = bytes > 2 * slot->bytes ? bytes : 2 * slot->bytes;
+        want = want > kScratchMin ? want : kScratchMin;
+    }
+    void* p = nullptr;
+    if (hipMallocFromPoolAsync(&p, want, ds->pool, stream) != hipSuccess || !p) {
+        (void)hipGetLastError();
+        return OSM_ENOMEM;
+    }
+    if (slot) {
+        if (slot->ptr) (void)hipFreeAsync(slot->ptr, stream);
+        slot->ptr = p;
+        slot->bytes = want;
+    }
+    *out = p;
+    return OSM_OK;
 }
 
 // ------------------------------------------------------------- validation
@@ -139,16 +192,13 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
     chunk = (chunk + E - 1) / E * E;
     S = (V + chunk - 1) / chunk;  // drop chunks that would start past the row
     if (N * S > kMaxDim) return OSM_EINVAL;
-    if (!ds->pool_ok) return OSM_ENOMEM;
     void* scratch = nullptr;
-    const size_t sbytes = (size_t)N * (size_t)S * 8;
-    if (hipMallocFromPoolAsync(&scratch, sbytes, ds->pool, stream) != hipSuccess || !scratch) {
-        (void)hipGetLastError();
-        return OSM_ENOMEM;
-    }
+    bool temp = false;
+    const int st = acquire_scratch(ds, stream, (size_t)N * (size_t)S * 8, &scratch, &temp);
+    if (st != OSM_OK) return st;
     hipError_t e = osm::launch_softmax_split(x, y, scratch, N, V, dtype, mode, S, chunk, vec,
                                              stream);
-    hipError_t f = hipFreeAsync(scratch, stream);
+    hipError_t f = temp ? hipFreeAsync(scratch, stream) : hipSuccess;
     if (e != hipSuccess) return OSM_EHIP;
     return hip_status(f);
 }
@@ -190,19 +240,15 @@ int launch_topk_pass(const void* x, float* vals, int32_t* idx, int64_t N, int64_
         a.waves_per_row = 4;
         return hip_status(osm::launch_topk(a, dtype, var));
     }
-    if (!ds->pool_ok) return OSM_ENOMEM;
     void* scratch = nullptr;
-    if (hipMallocFromPoolAsync(&scratch, osm::topk_part_bytes(N, S, K), ds->pool, stream) !=
-            hipSuccess ||
-        !scratch) {
-        (void)hipGetLastError();
-        return OSM_ENOMEM;
-    }
+    bool temp = false;
+    const int st = acquire_scratch(ds, stream, osm::topk_part_bytes(N, S, K), &scratch, &temp);
+    if (st != OSM_OK) return st;
     a.part = scratch;
     a.S = S;
     a.chunk = chunk;
     hipError_t e = osm::launch_topk(a, dtype, var);
-    hipError_t f = hipFreeAsync(scratch, stream);
+    hipError_t f = temp ? hipFreeAsync(scratch, stream) : hipSuccess;
     if (e != hipSuccess) return OSM_EHIP;
     return hip_status(f);
 }

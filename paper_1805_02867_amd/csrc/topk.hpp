@@ -25,12 +25,16 @@
 //    an element at or above it gets its key built and the exact key test
 //    (which settles ties by index).
 //  * Queue.  Elements that pass are appended to the wavefront's LDS queue
-//    right after its list (ballot + mbcnt compaction).
-//  * Select.  When the queue fills up, or holds enough entries to be worth
-//    raising tau, the wavefront selects the K largest keys of list + queue:
-//    K rounds of "largest key below the last one taken", each a scan of the
-//    occupied slots (one per lane per 64) and two 32-bit butterfly maxima.
-//    Lane k ends holding the k-th key, so the list stays sorted.
+//    right after its list (ballot + mbcnt compaction).  The region holds the
+//    list, a trigger's worth of queue and everything one step can append,
+//    so appends never overflow and never select.
+//  * Select.  After a step, when the queue holds enough entries to be worth
+//    raising tau, the wavefront selects the K largest keys of list + queue.
+//    Small K: K rounds of "largest key below the last one taken", each a
+//    scan of the occupied slots (one per lane per 64 slots) and two 32-bit
+//    butterfly maxima.  Large K: the list is kept sorted across the lanes
+//    and each 64-key chunk of the queue is sorted by a bitonic network and
+//    merged into it.  Either way lane k ends holding the k-th key.
 //  * Output.  The normalizer pairs are merged (Eq. 4) and the sorted list
 //    gives v_i = 2^{x_i log2e - s} / d and z_i = index, in key order.  With
 //    several wavefronts per row, wavefront 0 first selects the K largest keys
@@ -54,8 +58,8 @@ namespace osm {
 
 constexpr int TK_BLOCK = 256;
 constexpr int TK_KMAX = 64;            // largest supported K (one list slot per lane)
-constexpr int TK_REGION = 320;         // list + queue slots per wavefront
-constexpr int TK_PER_LANE = TK_REGION / 64;
+constexpr int TK_FLUSH_MAX = 64;       // largest selection trigger (queued keys)
+constexpr int TK_PER_LANE = 5;         // rows of 64 slots per K-round selection block
 // Selections with more than this many rounds use the sorting network.
 constexpr int TK_ROUNDS_MAX = 16;
 
@@ -68,8 +72,12 @@ __device__ __forceinline__ int flush_at(int K) {
     return 4 * K > 32 ? 4 * K : 32;
 }
 
-static_assert(TK_REGION % 64 == 0, "region must split evenly over 64 lanes");
-static_assert(TK_REGION - TK_KMAX >= 64, "the queue must take a full wavefront");
+// Slots of a wavefront's LDS region (list + queue) when at most `burst`
+// keys can be appended between two selection-trigger checks: the queue
+// holds fewer than TK_FLUSH_MAX keys at a check, so it never overflows and
+// appending never has to select (which keeps the selection code out of the
+// unrolled candidate paths).
+constexpr int region_slots(int burst) { return TK_KMAX + TK_FLUSH_MAX + burst; }
 
 __device__ __forceinline__ uint64_t make_key(float x, uint32_t idx) {
     uint32_t u = __float_as_uint(x);
@@ -260,6 +268,9 @@ struct TopkWave {
         int found;
         wave_sync();
         if (K <= TK_ROUNDS_MAX) {
+            // the occupied slots as rows of 64; the first block takes
+            // TK_PER_LANE rows, each further block the current list plus
+            // TK_PER_LANE - 1 more rows
             const int used = K + qcount;
             const int rows = (used + 63) >> 6;
             uint64_t e[TK_PER_LANE];
@@ -267,6 +278,15 @@ struct TopkWave {
             for (int j = 0; j < TK_PER_LANE; ++j)
                 e[j] = (j < rows && lane + 64 * j < used) ? region[lane + 64 * j] : 0ull;
             mine = select_topk<TK_PER_LANE>(e, rows, K, &found);
+            for (int r0 = TK_PER_LANE; r0 < rows; r0 += TK_PER_LANE - 1) {
+                e[0] = lane < K ? mine : 0ull;
+#pragma unroll
+                for (int j = 1; j < TK_PER_LANE; ++j) {
+                    const int r = r0 + j - 1;
+                    e[j] = (r < rows && lane + 64 * r < used) ? region[lane + 64 * r] : 0ull;
+                }
+                mine = select_topk<TK_PER_LANE>(e, TK_PER_LANE, K, &found);
+            }
         } else {
             uint64_t cur = lane < K ? region[lane] : 0ull;  // sorted list
             for (int c = 0; c < qcount; c += 64) {
@@ -307,17 +327,12 @@ struct TopkWave {
         }
     }
 
-    // Append the lanes' keys where p holds.
+    // Append the lanes' keys where p holds (the region is sized so that
+    // this always fits, see region_slots).
     __device__ __forceinline__ void append(bool p, uint64_t key) {
         uint64_t mask = __builtin_amdgcn_ballot_w64(p);
         if (mask == 0) return;
         int cnt = __builtin_popcountll(mask);
-        if (K + qcount + cnt > TK_REGION) {
-            flush();
-            p = p && key > tau;
-            mask = __builtin_amdgcn_ballot_w64(p);
-            cnt = __builtin_popcountll(mask);
-        }
         uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
                                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
         if (p) region[K + qcount + below] = key;
@@ -383,7 +398,9 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     constexpr int RB = WB / W;              // rows per workgroup
     constexpr int TR = 64 * W;              // threads per row
     constexpr int64_t STEP = (int64_t)TR * U;
-    __shared__ uint64_t region[WB][TK_REGION];
+    // one step appends at most U * E keys per lane
+    constexpr int REGION = region_slots(64 * U * E);
+    __shared__ uint64_t region[WB][REGION];
     __shared__ uint64_t published[WB];
     __shared__ MD wmd[WB];
     __shared__ float wmx[WB];
@@ -413,6 +430,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     const int64_t nvec = (L - head) / E;
     const int64_t tail0 = head + nvec * E;
     const u32x4* vb = reinterpret_cast<const u32x4*>(xr + head);
+    const int fa = flush_at(K);
 
     const u32x4 ninf = (E == 4) ? u32x4{0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u}
                                 : u32x4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
@@ -423,7 +441,6 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     // about to use.  The remaining vectors (fewer than a step) form one last
     // step with indices clamped into the row and masked after loading.
     const int64_t nfull = nvec / STEP;
-    const int fa = flush_at(K);
     const u32x4* lp = vb + tr;  // this lane's first vector
     // NT: the last read of the data (non-temporal hint)
     auto load_full = [&](u32x4 (&buf)[U], int64_t sidx, auto nt) {
@@ -515,6 +532,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
         float v[1] = {ok ? load1(xr + i) : -__builtin_inff()};
         if (ok) fold1(v[0]);
         tw.template offer<1>(v, base + (uint32_t)i, ok);
+        if (tw.qcount >= fa) tw.flush();
     }
     for (int64_t b0 = tail0; b0 < L; b0 += TR) {
         int64_t i = b0 + tr;
@@ -522,6 +540,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
         float v[1] = {ok ? load1(xr + i) : -__builtin_inff()};
         if (ok) fold1(v[0]);
         tw.template offer<1>(v, base + (uint32_t)i, ok);
+        if (tw.qcount >= fa) tw.flush();
     }
 
     // Bootstrap: the K-th largest distinct value among the lanes' maxima
@@ -664,7 +683,8 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_merge(const uint64_t* __restric
                                                       int32_t* __restrict__ idx, int64_t N,
                                                       int64_t S, int K) {
     constexpr int WB = TK_BLOCK / 64;
-    __shared__ uint64_t region[WB][TK_REGION];
+    constexpr int REGION = region_slots(64 * TK_MERGE_B);
+    __shared__ uint64_t region[WB][REGION];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int64_t row = (int64_t)blockIdx.x * WB + wv;
     if (lane < K) region[wv][lane] = 0;
@@ -681,10 +701,8 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_merge(const uint64_t* __restric
             k[b] = j < n ? pk[j] : 0ull;
         }
 #pragma unroll
-        for (int b = 0; b < TK_MERGE_B; ++b) {
-            tw.append(k[b] > tw.tau, k[b]);  // 0 (absent) never passes
-            if (tw.qcount >= fa) tw.flush();
-        }
+        for (int b = 0; b < TK_MERGE_B; ++b) tw.append(k[b] > tw.tau, k[b]);  // 0 never passes
+        if (tw.qcount >= fa) tw.flush();
     }
     tw.flush();
     const uint64_t key = tw.mine;
