@@ -205,13 +205,14 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
 
 // Top-k plan: one wavefront per row once the batch alone can give every
 // SIMD several wavefronts; a small batch of long rows is split into chunks
-// (a workgroup each, about four workgroups per CU in all); otherwise a
-// workgroup (four wavefronts) per row.
+// (a workgroup each, about two workgroups per CU in all: every chunk pays a
+// fixed selection cost, so more, shorter chunks stop paying off early);
+// otherwise a workgroup (four wavefronts) per row.
 Plan choose_topk(int64_t N, int64_t V, int cus) {
     if (N >= 4 * (int64_t)cus) return {OSM_KERNEL_ROWS, 64};
-    if (N < 2 * (int64_t)cus && V >= 16384) {
-        int64_t S = (4 * (int64_t)cus + N - 1) / N;
-        int64_t s_cap = V / 8192;  // keep chunks >= 8192 elements
+    if (N < 2 * (int64_t)cus && V >= 8192) {
+        int64_t S = (2 * (int64_t)cus + N - 1) / N;
+        int64_t s_cap = V / 4096;  // keep chunks >= 4096 elements
         if (S > s_cap) S = s_cap;
         if (S >= 2) return {OSM_KERNEL_SPLIT, S};
     }
