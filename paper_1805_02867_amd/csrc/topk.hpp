@@ -19,15 +19,17 @@
 //  * Bootstrap.  Before the first selection, tau comes from the first step:
 //    the K-th largest distinct value among the lanes' maxima is the value of
 //    K distinct elements, so every top-K element is at least as large.
-//  * Filter.  Per 16-byte vector, the maximum (needed for the online pair
-//    anyway) is compared with tau's value: most vectors are skipped with one
-//    compare.  Otherwise each element is compared with tau's value, and only
-//    an element at or above it gets its key built and the exact key test
-//    (which settles ties by index).
+//  * Filter.  Per step, the lane's maximum over its vectors (which also
+//    drives the rescale test of the online pair) is compared with tau's
+//    value: most steps are skipped with one compare per lane.  Otherwise
+//    each vector's maximum, then each element, is compared with tau's value,
+//    and only an element at or above it gets its key built and the exact key
+//    test (which settles ties by index).
 //  * Queue.  Elements that pass are appended to the wavefront's LDS queue
 //    right after its list (ballot + mbcnt compaction).  The region holds the
-//    list, a trigger's worth of queue and everything one step can append,
-//    so appends never overflow and never select.
+//    list, a trigger's worth of queue and everything that can be appended
+//    between two trigger checks (half a step), so appends never overflow and
+//    never select.
 //  * Select.  After a step, when the queue holds enough entries to be worth
 //    raising tau, the wavefront selects the K largest keys of list + queue.
 //    Small K: K rounds of "largest key below the last one taken", each a
@@ -353,6 +355,27 @@ struct TopkWave {
     }
 };
 
+// Largest of three binary32 values in one instruction.  fmaxf on loaded
+// values makes the compiler quiet possible signalling NaNs first (two extra
+// instructions per pair in IEEE mode); here a NaN input may give NaN, which
+// only concerns rows holding NaN, whose top-k is unspecified (their outputs
+// are NaN through the normalizer in any case).
+__device__ __forceinline__ float max3_raw(float a, float b, float c) {
+    float r;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+
+// max(acc, x[0..N-1]) by a chain of three-input maxima.
+template <int N>
+__device__ __forceinline__ float vec_max_into(const float (&x)[N], float acc) {
+    static_assert(N % 2 == 0, "vectors hold an even number of elements");
+    float r = max3_raw(x[0], x[1], acc);
+#pragma unroll
+    for (int i = 2; i < N; i += 2) r = max3_raw(r, x[i], x[i + 1]);
+    return r;
+}
+
 // Raw 16-byte vector and its widening to binary32.
 template <typename T>
 __device__ __forceinline__ void widen(u32x4 q, float (&x)[Vec<T>::N]) {
@@ -398,8 +421,11 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     constexpr int RB = WB / W;              // rows per workgroup
     constexpr int TR = 64 * W;              // threads per row
     constexpr int64_t STEP = (int64_t)TR * U;
-    // one step appends at most U * E keys per lane
-    constexpr int REGION = region_slots(64 * U * E);
+    // The candidate path checks the selection trigger after its first UH
+    // vectors and again at the end of the step, so at most
+    // max(UH, U - UH) * E keys per lane are appended between two checks.
+    constexpr int UH = U / 2;
+    constexpr int REGION = region_slots(64 * E * (UH > U - UH ? UH : U - UH));
     __shared__ uint64_t region[WB][REGION];
     __shared__ uint64_t published[WB];
     __shared__ MD wmd[WB];
@@ -461,7 +487,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
         for (int u = 0; u < U; ++u) {
             float xv[E];
             widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
-            lm = fmaxf(lm, vec_max(xv));
+            lm = vec_max_into(xv, lm);
         }
         return lm;
     };
@@ -469,9 +495,13 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
 #pragma unroll
     for (int u = 0; u < U; ++u) all_ok[u] = true;
 
-    MD st[U];
+    // The lane's normalizer: one reference sr shared by U partial sums
+    // dacc[u] (independent chains for the exponentials of a step), so that
+    // d = sum_u dacc[u] relative to sr.
+    float sr = kEmptyS;
+    float dacc[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) st[u] = md_empty();
+    for (int u = 0; u < U; ++u) dacc[u] = 0.0f;
 
     // Safe variant: the row's maximum first (plain loads, so that the second
     // read may still find the data in cache), then s = max * log2e is held
@@ -517,12 +547,21 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
         // reach d as NaN, as in the online pair
         sfix = mx * kLog2e;
         if (!(sfix > kEmptyS)) sfix = kEmptyS;
-#pragma unroll
-        for (int u = 0; u < U; ++u) st[u] = MD{sfix, 0.0f};
+        sr = sfix;
     }
+    // Online: move the reference to t (rescaling every partial sum) when t
+    // exceeds it by more than kLazy; every term then stays <= 2^kLazy.
+    auto raise_ref = [&](float t) {
+        if (t > sr + kLazy) {
+            const float f = exp2_hw(sr - t);
+#pragma unroll
+            for (int u = 0; u < U; ++u) dacc[u] *= f;
+            sr = t;
+        }
+    };
     auto fold1 = [&](float v) {
-        if constexpr (VAR == TK_ONLINE) st[0] = md_fold1(st[0], v);
-        else if constexpr (VAR == TK_SAFE) st[0].d += exp2_hw(__builtin_fmaf(v, kLog2e, -sfix));
+        if constexpr (VAR == TK_ONLINE) raise_ref(v * kLog2e);
+        if constexpr (VAR != TK_VALUES) dacc[0] += exp2_hw(__builtin_fmaf(v, kLog2e, -sr));
     };
 
     // scalar head and tail: wave-uniform loops, one element per lane
@@ -569,29 +608,35 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
             if (kth != 0) tw.raise_tau((kth & 0xFFFFFFFF00000000ull) - 1);
         }
     };
-    // One step: fold every vector, then (one test per step) offer the vectors
-    // that may hold a candidate.
+    // One step: the lane's maximum over the step (one rescale test, and one
+    // candidate test, per step), the exponentials of every element, then the
+    // vectors that may hold a candidate are offered.
     auto step = [&](const u32x4 (&buf)[U], const bool (&ok)[U], int64_t b0, bool masked) {
-        float mxs[U];
-        float lane_mx = -__builtin_inff();
+        const float lane_mx = lane_max_of(buf, ok, masked);
+        if constexpr (VAR == TK_ONLINE) {
+            // a wave-uniform branch, so that the common case skips the
+            // rescale instead of computing it and selecting it away
+            const float t = lane_mx * kLog2e;
+            if (__builtin_amdgcn_ballot_w64(t > sr + kLazy) != 0) raise_ref(t);
+        }
+        if constexpr (VAR != TK_VALUES) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            float xv[E];
-            widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
-            mxs[u] = vec_max(xv);
-            lane_mx = fmaxf(lane_mx, mxs[u]);
-            if constexpr (VAR == TK_ONLINE) st[u] = md_fold_lazy(st[u], xv, mxs[u]);
-            else if constexpr (VAR == TK_SAFE) st[u].d = sum_exp_fixed(st[u].d, xv, sfix);
+            for (int u = 0; u < U; ++u) {
+                float xv[E];
+                widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
+                dacc[u] = sum_exp_fixed(dacc[u], xv, sr);
+            }
         }
         if (__builtin_amdgcn_ballot_w64(lane_mx >= tw.tau_v) != 0) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                if (__builtin_amdgcn_ballot_w64(ok[u] && mxs[u] >= tw.tau_v) != 0) {
-                    float xv[E];
-                    widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
+                float xv[E];
+                widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
+                if (__builtin_amdgcn_ballot_w64(ok[u] && vec_max(xv) >= tw.tau_v) != 0) {
                     const int64_t e0 = head + (b0 + (int64_t)u * TR + tr) * E;
                     tw.template offer<E>(xv, base + (uint32_t)e0, ok[u]);
                 }
+                if (UH > 0 && u == UH - 1 && tw.qcount >= fa) tw.flush();
             }
         }
         if (tw.qcount >= fa) tw.flush();
@@ -635,11 +680,12 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
 
     // merge of the normalizer pairs: wavefront butterflies, then (W > 1)
     // a fixed-order merge of the row's wavefronts
-    MD md = st[0];
+    MD md = md_empty();
     if constexpr (VAR != TK_VALUES) {
+        float dsum = dacc[0];
 #pragma unroll
-        for (int u = 1; u < U; ++u) md = md_merge(md, st[u]);
-        md = group_merge<64>(md);
+        for (int u = 1; u < U; ++u) dsum += dacc[u];
+        md = group_merge<64>(MD{sr, dsum});
     }
     uint64_t key = tw.mine;
     if constexpr (W > 1) {
@@ -726,7 +772,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_merge(const uint64_t* __restric
 // loads in flight per wavefront without pushing the register count (and so
 // the occupancy) down; bfloat16 vectors widen to twice the registers.
 #ifndef OSM_TOPK_U1
-#define OSM_TOPK_U1 4
+#define OSM_TOPK_U1 5
 #endif
 #ifndef OSM_TOPK_U1B
 #define OSM_TOPK_U1B 2
