@@ -13,7 +13,8 @@ The printed JSON line reports the step's algorithmic bytes per second
 per-kernel breakdown timed with HIP events on the launch stream, the roofline
 entry of the dominant kernel, and the oracle timed on the host cores.  The
 naive and safe modes are timed on the same batch after the steps, for the
-paper's memory-access comparison, and so are the paper's four softmax + top-k
+paper's memory-access comparison (with the row-resident variant, one load and
+one store per element, reported apart), and so are the paper's four softmax + top-k
 algorithms (online fused, safe fused, online unfused, safe unfused), with a
 plain copy and a plain read as reference kernels.
 
@@ -173,7 +174,10 @@ def sweep(path: str):
         es = 2 if dt == "bf16" else 4
         y = torch.empty_like(x)
         est = 12.0 * N * V / 6e3 / 1e3  # us at ~6 TB/s
-        for mode, acc in (("online", 3), ("safe", 4), ("naive", 3)):
+        modes = [("online", 3), ("safe", 4), ("naive", 3)]
+        if V // (16 // es) <= osm.RESIDENT_MAX_VEC:
+            modes.append(("resident", 2))
+        for mode, acc in modes:
             us = run(lambda m=mode: osm.softmax_fwd(x, y, mode=m), est)
             emit({"workload": name, "op": f"softmax_{mode}", "N": N, "V": V, "dtype": dt,
                   "plan": list(osm.plan(N, V, x.dtype, mode)), "us": round(us, 2),
@@ -296,7 +300,9 @@ def main():
 
     # the paper's comparison: naive and safe on the same batch
     compare = {}
-    for mode, nbytes in (("naive", 12.0), ("safe", 16.0), ("online", 12.0)):
+    # (and the row-resident variant, one load + one store: 8 B/element,
+    # reported apart from the paper's three modes)
+    for mode, nbytes in (("naive", 12.0), ("safe", 16.0), ("online", 12.0), ("resident", 8.0)):
         t = timed_calls(lambda m=mode: osm.softmax_fwd(x, y, mode=m), args.compare_reps, stream)
         compare[mode] = {"median_us": round(median(t) * 1e3, 2),
                          "p10_us": round(pct(t, 0.1) * 1e3, 2),

@@ -62,8 +62,17 @@ enum osm_dtype { OSM_F32 = 0, OSM_BF16 = 1 };
  *              loads and one store per element.
  *  OSM_ONLINE: Alg. 3 -- one pass carrying the running (max, normalizer)
  *              pair merged with Eq. 4, then the output pass.  Two loads and
- *              one store per element. */
-enum osm_mode { OSM_NAIVE = 0, OSM_SAFE = 1, OSM_ONLINE = 2 };
+ *              one store per element.
+ *  OSM_RESIDENT: Alg. 3's pair (per lane, then merged with Eq. 4) with the
+ *              row held in registers between the normalizer and the output:
+ *              one load and one store per element.  Rows of at most
+ *              OSM_RESIDENT_MAX_VEC whole 16-byte vectors (65536 binary32 or
+ *              131072 bfloat16 elements, plus up to one partial vector at
+ *              each end); longer rows give OSM_EUNSUPPORTED. */
+enum osm_mode { OSM_NAIVE = 0, OSM_SAFE = 1, OSM_ONLINE = 2, OSM_RESIDENT = 3 };
+
+/* Longest row of OSM_RESIDENT, in 16-byte vectors. */
+#define OSM_RESIDENT_MAX_VEC 16384
 
 /* Status codes. */
 enum osm_status {
@@ -120,12 +129,14 @@ enum osm_topk_algo {
  * function (Theorem 1) and differ in their passes over memory.
  * Errors: OSM_EINVAL for N < 0, V < 1, sizes above the limits, null pointers
  * with N > 0, unknown dtype or mode, misaligned or overlapping buffers.
- * OSM_ENOMEM if the split-V scratch array cannot be allocated. */
+ * OSM_ENOMEM if the split-V scratch array cannot be allocated.
+ * OSM_EUNSUPPORTED for OSM_RESIDENT rows longer than it holds. */
 OSM_API int softmax_fwd(const void* x, void* y, int64_t N, int64_t V, int dtype, int mode,
                 hipStream_t stream);
 
 /* softmax_fwd with an explicit kernel family and parameter (osm_kernel);
- * OSM_KERNEL_AUTO ignores param.  Results agree with softmax_fwd within the
+ * OSM_KERNEL_AUTO ignores param.  OSM_RESIDENT accepts OSM_KERNEL_AUTO or
+ * OSM_KERNEL_ROWS with param = 256, 512 or 1024 threads per row.  Results agree with softmax_fwd within the
  * library's accuracy (binary32 rounding differs with the reduction tree).
  * Errors: as softmax_fwd, plus OSM_EINVAL for an unknown kernel or a param
  * it does not accept. */
@@ -183,7 +194,8 @@ OSM_API int topk_fwd(const void* x, float* vals, int32_t* idx, int64_t N, int64_
                      int dtype, hipStream_t stream);
 
 /* Kernel family and parameter softmax_fwd would use for this shape on the
- * current device.  Errors: OSM_EINVAL for bad sizes, dtype or null outputs. */
+ * current device (for OSM_RESIDENT: OSM_KERNEL_ROWS and the threads per row).  Errors: OSM_EINVAL for bad sizes, dtype or
+ * null outputs; OSM_EUNSUPPORTED for OSM_RESIDENT rows it cannot hold. */
 OSM_API int osm_plan(int64_t N, int64_t V, int dtype, int mode, int* kernel, int64_t* param);
 
 /* Kernel family and parameter the top-k entry points would use for this

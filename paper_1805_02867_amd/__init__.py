@@ -15,7 +15,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libosoftmax.so")
 
 F32, BF16 = 0, 1
-NAIVE, SAFE, ONLINE = 0, 1, 2
+NAIVE, SAFE, ONLINE, RESIDENT = 0, 1, 2, 3
+RESIDENT_MAX_VEC = 16384
 KERNEL_AUTO, KERNEL_ROWS, KERNEL_SPLIT = 0, 1, 2
 OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM = 0, 1, 2, 3, 4
 TOPK_KMAX = 64
@@ -25,7 +26,7 @@ TOPK_ALGOS = {"online_fused": TOPK_ONLINE_FUSED, "safe_fused": TOPK_SAFE_FUSED,
               "values": TOPK_VALUES}
 UNFUSED = (TOPK_SAFE_UNFUSED, TOPK_ONLINE_UNFUSED)
 
-MODES = {"naive": NAIVE, "safe": SAFE, "online": ONLINE}
+MODES = {"naive": NAIVE, "safe": SAFE, "online": ONLINE, "resident": RESIDENT}
 _DTYPES = {torch.float32: F32, torch.bfloat16: BF16}
 
 _lib = None

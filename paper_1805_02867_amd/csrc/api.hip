@@ -154,6 +154,26 @@ Plan choose(int64_t N, int64_t V, int dtype, int cus) {
     return {OSM_KERNEL_ROWS, 1024};
 }
 
+// Row-resident mode: the first (block, 16-byte vectors per lane) shape that
+// holds the row's vectors; false if none does.  Smaller workgroups come
+// first: with 16 vectors per lane (4 wavefronts per SIMD) a CU then holds two
+// or four rows at once, so one row's loads overlap another's reduction.
+struct ResShape {
+    int block, r;
+};
+bool choose_resident(int64_t V, int dtype, int64_t block_req, ResShape* out) {
+    const int64_t need = V / elems_per_vec(dtype);  // at least the row's whole vectors
+    static const ResShape shapes[] = {{256, 4}, {256, 8}, {256, 16}, {512, 16}, {1024, 16}};
+    for (const ResShape& c : shapes) {
+        if (block_req && c.block != block_req) continue;
+        if (need <= (int64_t)c.block * c.r) {
+            *out = c;
+            return true;
+        }
+    }
+    return false;
+}
+
 bool team_ok(int64_t t) {
     return t == 4 || t == 8 || t == 16 || t == 32 || t == 64 || t == 128 || t == 256 ||
            t == 512 || t == 1024;
@@ -163,17 +183,31 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
                 int64_t param, hipStream_t stream) {
     size_t bytes = 0;
     if (!check_shape(N, V, dtype, &bytes)) return OSM_EINVAL;
-    if (mode != OSM_NAIVE && mode != OSM_SAFE && mode != OSM_ONLINE) return OSM_EINVAL;
+    if (mode != OSM_NAIVE && mode != OSM_SAFE && mode != OSM_ONLINE && mode != OSM_RESIDENT)
+        return OSM_EINVAL;
     if (kernel != OSM_KERNEL_AUTO && kernel != OSM_KERNEL_ROWS && kernel != OSM_KERNEL_SPLIT)
         return OSM_EINVAL;
-    if (kernel == OSM_KERNEL_ROWS && !team_ok(param)) return OSM_EINVAL;
-    if (kernel == OSM_KERNEL_SPLIT && (param < 1 || param > kMaxDim)) return OSM_EINVAL;
+    if (mode == OSM_RESIDENT) {
+        if (kernel == OSM_KERNEL_SPLIT ||
+            (kernel == OSM_KERNEL_ROWS && param != 256 && param != 512 && param != 1024))
+            return OSM_EINVAL;
+    } else {
+        if (kernel == OSM_KERNEL_ROWS && !team_ok(param)) return OSM_EINVAL;
+        if (kernel == OSM_KERNEL_SPLIT && (param < 1 || param > kMaxDim)) return OSM_EINVAL;
+    }
     if (N == 0) return OSM_OK;
     if (!x || !y) return OSM_EINVAL;
     const size_t es = elem_size(dtype);
     if (!aligned(x, es) || !aligned(y, es)) return OSM_EINVAL;
     if (overlaps(x, bytes, y, bytes)) return OSM_EINVAL;
     const bool vec = (((uintptr_t)x - (uintptr_t)y) % 16) == 0;
+    if (mode == OSM_RESIDENT) {
+        ResShape rs;
+        if (!choose_resident(V, dtype, kernel == OSM_KERNEL_ROWS ? param : 0, &rs))
+            return OSM_EUNSUPPORTED;
+        return hip_status(
+            osm::launch_softmax_resident(x, y, N, V, dtype, rs.block, rs.r, vec, stream));
+    }
 
     int dev = 0;
     DeviceState* ds = device_state(&dev);
@@ -368,8 +402,16 @@ int osm_topk_plan(int64_t N, int64_t V, int dtype, int K, int* kernel, int64_t* 
 int osm_plan(int64_t N, int64_t V, int dtype, int mode, int* kernel, int64_t* param) {
     size_t bytes = 0;
     if (!check_shape(N, V, dtype, &bytes)) return OSM_EINVAL;
-    if (mode != OSM_NAIVE && mode != OSM_SAFE && mode != OSM_ONLINE) return OSM_EINVAL;
+    if (mode != OSM_NAIVE && mode != OSM_SAFE && mode != OSM_ONLINE && mode != OSM_RESIDENT)
+        return OSM_EINVAL;
     if (!kernel || !param) return OSM_EINVAL;
+    if (mode == OSM_RESIDENT) {
+        ResShape rs;
+        if (!choose_resident(V, dtype, 0, &rs)) return OSM_EUNSUPPORTED;
+        *kernel = OSM_KERNEL_ROWS;
+        *param = rs.block;
+        return OSM_OK;
+    }
     DeviceState* ds = device_state(nullptr);
     Plan p = choose(N, V, dtype, ds ? ds->cus : 256);
     *kernel = p.kernel;

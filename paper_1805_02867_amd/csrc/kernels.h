@@ -18,6 +18,12 @@ hipError_t launch_softmax_split(const void* x, void* y, void* scratch, int64_t N
                                 int dtype, int mode, int64_t S, int64_t chunk, bool vec,
                                 hipStream_t st);
 
+// Row-resident online softmax: one row per workgroup of `block` threads,
+// r 16-byte vectors per lane held in registers; vec: y congruent with x
+// modulo 16 bytes (vector stores), else outputs stored one by one.
+hipError_t launch_softmax_resident(const void* x, void* y, int64_t N, int64_t V, int dtype,
+                                   int block, int r, bool vec, hipStream_t st);
+
 // What the top-k kernels compute next to the selection (Section 4, and the
 // comparisons of Section 5.2):
 //  TK_ONLINE: the online pair, one pass (Alg. 4);

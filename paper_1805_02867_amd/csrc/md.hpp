@@ -275,6 +275,53 @@ __device__ __forceinline__ float group_sum(float v) {
     }
 }
 
+// ------------------------------------------------------------ team reductions
+// TEAM <= 64: butterflies inside the lane group.  TEAM > 64 (= the whole
+// workgroup): wavefront butterflies, then every thread merges the W
+// per-wavefront values from LDS in wavefront order, so all threads hold the
+// same bits.
+template <int TEAM>
+struct Team {
+    static constexpr int W = TEAM > 64 ? TEAM / 64 : 1;
+    struct Smem {
+        MD md[W];
+        float f[W];
+    };
+
+    __device__ __forceinline__ static MD merge(MD a, Smem& sm) {
+        if constexpr (TEAM <= 64) {
+            return group_merge<TEAM>(a);
+        } else {
+            MD w = group_merge<64>(a);
+            int wave = threadIdx.x >> 6;
+            if ((threadIdx.x & 63) == 0) sm.md[wave] = w;
+            __syncthreads();
+            MD r = sm.md[0];
+#pragma unroll
+            for (int i = 1; i < W; ++i) r = md_merge(r, sm.md[i]);
+            __syncthreads();
+            return r;
+        }
+    }
+
+    template <bool IS_MAX>
+    __device__ __forceinline__ static float reduce(float a, Smem& sm) {
+        if constexpr (TEAM <= 64) {
+            return IS_MAX ? group_max<TEAM>(a) : group_sum<TEAM>(a);
+        } else {
+            float w = IS_MAX ? group_max<64>(a) : group_sum<64>(a);
+            int wave = threadIdx.x >> 6;
+            if ((threadIdx.x & 63) == 0) sm.f[wave] = w;
+            __syncthreads();
+            float r = sm.f[0];
+#pragma unroll
+            for (int i = 1; i < W; ++i) r = IS_MAX ? fmaxf(r, sm.f[i]) : r + sm.f[i];
+            __syncthreads();
+            return r;
+        }
+    }
+};
+
 // Keep LDS traffic between lanes of one wavefront in program order.
 __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

@@ -66,7 +66,7 @@ X, Y = 0x10000000, 0x20000000
     (X, Y, 4, 1 << 31, 0, 2),      # V too large
     (X, Y, 1 << 31, 4, 0, 2),      # N too large
     (X, Y, 4, 10, 2, 2),           # unknown dtype
-    (X, Y, 4, 10, 0, 3),           # unknown mode
+    (X, Y, 4, 10, 0, 4),           # unknown mode
     (0, Y, 4, 10, 0, 2),           # null x
     (X, 0, 4, 10, 0, 2),           # null y
     (X, X + 8, 4, 10, 0, 2),       # overlap
@@ -85,6 +85,38 @@ def test_n_zero_is_a_noop():
 @pytest.mark.parametrize("kernel,param", [(7, 0), (1, 3), (1, 2048), (1, 0), (2, 0), (2, -5)])
 def test_softmax_fwd_ex_rejects(kernel, param):
     assert osm.lib().softmax_fwd_ex(X, Y, 4, 10, 0, 2, kernel, param, None) == osm.EINVAL
+
+
+def test_resident_rejects_rows_it_cannot_hold():
+    """OSM_RESIDENT holds at most OSM_RESIDENT_MAX_VEC whole 16-byte vectors
+    per row; longer rows are refused before any launch."""
+    big = osm.RESIDENT_MAX_VEC * 4 + 4          # binary32: one vector too many
+    assert osm.lib().softmax_fwd(X, Y, 4, big, 0, osm.RESIDENT, None) == osm.EUNSUPPORTED
+    bigb = osm.RESIDENT_MAX_VEC * 8 + 8         # bfloat16
+    assert osm.lib().softmax_fwd(X, Y, 4, bigb, 1, osm.RESIDENT, None) == osm.EUNSUPPORTED
+    # a forced workgroup size that cannot hold the row
+    assert osm.lib().softmax_fwd_ex(X, Y, 4, 32000, 0, osm.RESIDENT, osm.KERNEL_ROWS, 256,
+                                    None) == osm.EUNSUPPORTED
+    k = ctypes.c_int()
+    p = ctypes.c_int64()
+    assert osm.lib().osm_plan(4, big, 0, osm.RESIDENT, ctypes.byref(k),
+                              ctypes.byref(p)) == osm.EUNSUPPORTED
+    assert osm.lib().osm_plan(4, 32000, 0, osm.RESIDENT, ctypes.byref(k), ctypes.byref(p)) == osm.OK
+    assert (k.value, p.value) == (osm.KERNEL_ROWS, 512)
+    assert osm.lib().osm_plan(4, 128256, 1, osm.RESIDENT, ctypes.byref(k), ctypes.byref(p)) == osm.OK
+    assert (k.value, p.value) == (osm.KERNEL_ROWS, 1024)
+
+
+@pytest.mark.parametrize("kernel,param", [(2, 4), (1, 64), (1, 128), (1, 2048), (7, 0)])
+def test_resident_rejects_other_kernels(kernel, param):
+    assert osm.lib().softmax_fwd_ex(X, Y, 4, 1000, 0, osm.RESIDENT, kernel, param,
+                                    None) == osm.EINVAL
+
+
+def test_resident_limit_matches_header():
+    text = open(HEADER).read()
+    assert re.search(rf"#define OSM_RESIDENT_MAX_VEC {osm.RESIDENT_MAX_VEC}\b", text)
+    assert re.search(rf"\bOSM_RESIDENT\s*=\s*{osm.RESIDENT}\b", text)
 
 
 V_, I_ = 0x30000000, 0x40000000
@@ -152,6 +184,7 @@ def test_plan_rejects_bad_shapes():
     assert osm.lib().osm_plan(4, 0, 0, 2, ctypes.byref(k), ctypes.byref(p)) == osm.EINVAL
     assert osm.lib().osm_plan(4, 10, 5, 2, ctypes.byref(k), ctypes.byref(p)) == osm.EINVAL
     assert osm.lib().osm_plan(4, 10, 0, 9, ctypes.byref(k), ctypes.byref(p)) == osm.EINVAL
+    assert osm.lib().osm_plan(4, 10, 0, 4, ctypes.byref(k), ctypes.byref(p)) == osm.EINVAL
     assert osm.lib().osm_plan(4, 10, 0, 2, None, ctypes.byref(p)) == osm.EINVAL
 
 
