@@ -16,6 +16,8 @@ bfloat16 given as raw ``uint16`` bit patterns with ``dtype="bf16"``):
 * :func:`topk`           -- Eq. 5 by a full sort, ties to the lower index.
 * :func:`topk_alg4`      -- the fused single pass of Alg. 4 (Section 4).
 * :func:`bf16_round`     -- binary64 -> bfloat16, round to nearest even.
+* :func:`proj`           -- the projection ahead of the softmax (Section 1):
+  logits = h . w^T in binary64.
 """
 from __future__ import annotations
 
@@ -59,6 +61,8 @@ class Oracle:
         for name in ("orc_topk", "orc_topk_alg4"):
             getattr(lib, name).argtypes = [vp, i32, i64, i64, i32, vp, vp]
             getattr(lib, name).restype = i32
+        lib.orc_proj.argtypes = [vp, i32, vp, i32, i64, i64, i64, vp]
+        lib.orc_proj.restype = i32
         lib.orc_md_combine.argtypes = [ctypes.c_double] * 4 + [vp, vp]
         lib.orc_md_combine.restype = None
         lib.orc_bf16_round.argtypes = [vp, i64, vp]
@@ -133,6 +137,18 @@ class Oracle:
         _check(self.lib.orc_topk_alg4(_ptr(x), dt, n, v, int(k), _ptr(vals), _ptr(idx)),
                "topk_alg4")
         return vals, idx
+
+    def proj(self, h: np.ndarray, w: np.ndarray, hdtype: str | None = None,
+             wdtype: str | None = None) -> np.ndarray:
+        """logits[n][v] = sum_k h[n][k] w[v][k] in binary64 (h: N x H,
+        w: V x H; each float32, float64 or bfloat16 patterns)."""
+        h, hdt, n, hh = _prep(h, hdtype)
+        w, wdt, v, hw = _prep(w, wdtype)
+        if hh != hw:
+            raise ValueError("h and w must have the same number of columns")
+        out = np.empty((n, v), np.float64)
+        _check(self.lib.orc_proj(_ptr(h), hdt, _ptr(w), wdt, n, hh, v, _ptr(out)), "proj")
+        return out
 
     def bf16_round(self, y: np.ndarray) -> np.ndarray:
         """binary64 -> bfloat16 bit patterns (uint16), round to nearest, ties to
@@ -229,6 +245,10 @@ def topk_alg4(x, k, dtype=None):
 
 def bf16_round(y):
     return _get().bf16_round(y)
+
+
+def proj(h, w, hdtype=None, wdtype=None):
+    return _get().proj(h, w, hdtype, wdtype)
 
 
 def bf16_to_f64(bits: np.ndarray) -> np.ndarray:

@@ -324,3 +324,28 @@ static uint16_t bf16_from_f64(double a) {
 void orc_bf16_round(const double* y, int64_t n, uint16_t* out) {
     for (int64_t i = 0; i < n; ++i) out[i] = bf16_from_f64(y[i]);
 }
+
+/* ------------------------------------------------------------ projection */
+/* The projection layer that precedes the softmax in a language model
+ * (Section 1; the Discussion proposes fusing the softmax into it):
+ *   logits[n][v] = sum_{k < H} h[n][k] * w[v][k]
+ * for hidden vectors h (N x H) and a weight matrix w (V x H, one row per
+ * vocabulary entry), accumulated in binary64 with k ascending.  Products of
+ * bfloat16 or binary32 inputs are exact in binary64. */
+int orc_proj(const void* h, int hdtype, const void* w, int wdtype, int64_t N, int64_t H,
+             int64_t V, double* out) {
+    if (bad_args(h, hdtype, N, H) || bad_args(w, wdtype, V, H) || (N > 0 && !out))
+        return ORC_EINVAL;
+#pragma omp parallel for schedule(dynamic, 1) num_threads(orc_get_threads())
+    for (int64_t n = 0; n < N; ++n) {
+        const void* hr = row_ptr(h, hdtype, H, n);
+        double* o = out + (size_t)n * (size_t)V;
+        for (int64_t v = 0; v < V; ++v) {
+            const void* wr = row_ptr(w, wdtype, H, v);
+            double acc = 0.0;
+            for (int64_t k = 0; k < H; ++k) acc += load_elem(hr, hdtype, k) * load_elem(wr, wdtype, k);
+            o[v] = acc;
+        }
+    }
+    return ORC_OK;
+}

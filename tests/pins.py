@@ -292,10 +292,41 @@ def check_golden(orc):
                                            err_msg=name)
 
 
+def check_projection(orc):
+    """The projection h . w^T against: integer arithmetic (small-integer inputs
+    make every sum exact), numpy's matmul, the identity matrix, linearity in
+    w, and bfloat16 inputs widened exactly."""
+    rng = _rng(31)
+    # exact: small integers scaled by powers of two
+    h = (rng.integers(-4, 5, (7, 37)) * 0.125).astype(np.float32)
+    w = (rng.integers(-4, 5, (11, 37)) * 0.0625).astype(np.float32)
+    want = (np.rint(h * 8).astype(np.int64) @ np.rint(w * 16).astype(np.int64).T) / 128.0
+    assert np.array_equal(orc.proj(h, w), want)
+    # a library matmul on random inputs, non-square (a transposed operand fails)
+    h = rng.standard_normal((5, 23)).astype(np.float32)
+    w = rng.standard_normal((13, 23)).astype(np.float32)
+    got = orc.proj(h, w)
+    ref = h.astype(np.float64) @ w.astype(np.float64).T
+    assert got.shape == (5, 13)
+    np.testing.assert_allclose(got, ref, rtol=1e-13, atol=1e-13)
+    # identity weights give the hidden vectors back
+    assert np.array_equal(orc.proj(h, np.eye(23, dtype=np.float32)), h.astype(np.float64))
+    # linearity: doubling w doubles every logit exactly
+    assert np.array_equal(orc.proj(h, 2 * w), 2 * orc.proj(h, w))
+    # bfloat16 inputs: the same as their exact binary32 widening
+    hb = torch.from_numpy(h).to(torch.bfloat16)
+    wb = torch.from_numpy(w).to(torch.bfloat16)
+    hbits = hb.view(torch.int16).numpy().view(np.uint16)
+    wbits = wb.view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(orc.proj(hbits, wbits, "bf16", "bf16"),
+                          orc.proj(hb.float().numpy(), wb.float().numpy()))
+
+
 ALL = [
     check_softmax_decimal, check_softmax_bf16_input, check_softmax_sums_to_one,
     check_softmax_closed_forms, check_softmax_shift_and_overflow,
     check_softmax_nonfinite, check_theorem1, check_prefix_bound,
     check_combine_algebra, check_topk_enumeration, check_topk_library,
     check_topk_alg4, check_topk_signed_zero, check_bf16_rounding, check_golden,
+    check_projection,
 ]

@@ -64,6 +64,15 @@ MUTANTS = {
     "bf16_subnormal_spacing": (
         "if (ex < -126) ex = -126;",
         "if (ex < -127) ex = -127;"),
+    "proj_transposed_weight_index": (
+        "acc += load_elem(hr, hdtype, k) * load_elem(wr, wdtype, k);",
+        "acc += load_elem(hr, hdtype, k) * load_elem(row_ptr(w, wdtype, H, k % V), wdtype, v % H);"),
+    "proj_skips_last_term": (
+        "for (int64_t k = 0; k < H; ++k) acc += load_elem(hr, hdtype, k)",
+        "for (int64_t k = 0; k + 1 < H; ++k) acc += load_elem(hr, hdtype, k)"),
+    "proj_squares_hidden": (
+        "acc += load_elem(hr, hdtype, k) * load_elem(wr, wdtype, k);",
+        "acc += load_elem(hr, hdtype, k) * load_elem(hr, hdtype, k);"),
     "bf16_widening_wrong_shift": (
         "uint32_t bits = (uint32_t)((const uint16_t*)row)[i] << 16;",
         "uint32_t bits = (uint32_t)((const uint16_t*)row)[i] << 15;"),
