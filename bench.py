@@ -14,7 +14,8 @@ per-kernel breakdown timed with HIP events on the launch stream, the roofline
 entry of the dominant kernel, and the oracle timed on the host cores.  The
 naive and safe modes are timed on the same batch after the steps, for the
 paper's memory-access comparison (with the row-resident variant, one load and
-one store per element, reported apart), and so are the paper's four softmax + top-k
+one store per element, reported apart), the projection with softmax + top-k in
+its epilogue (against the projection writing logits), and the paper's four softmax + top-k
 algorithms (online fused, safe fused, online unfused, safe unfused), with a
 plain copy and a plain read as reference kernels.
 
@@ -35,6 +36,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, decimal GB/s
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bfloat16 matrix peak
 N_ROWS, V_LEN, SIGMA, SHIFT_FRAC, K_TOP = 4000, 32000, 2.0, 0.01, 5
 WORKLOAD = "online softmax + fused softmax/top-5, 4000x32000 fp32 N(0,2), 1% rows +1000"
 
@@ -95,6 +97,41 @@ def queued_batches(fn, reps: int, batches: int, stream):
         b.record(stream)
         torch.cuda.synchronize()
         out.append(a.elapsed_time(b) * 1e3 / reps)
+    return out
+
+
+def proj_compare(osm, torch, N, H, V, K, reps, stream):
+    """The projection (bfloat16 h: N x H, w: V x H) with softmax + top-K in its
+    epilogue, against the two-kernel path (the same projection writing binary32
+    logits, then the fused top-K) and against torch's bfloat16 matmul (a
+    library GEMM) followed by the fused top-K.  Times are medians per call."""
+    g = torch.Generator(device="cuda").manual_seed(0)
+    h = torch.randn(N, H, device="cuda", generator=g).to(torch.bfloat16)
+    w = (torch.randn(V, H, device="cuda", generator=g) / H ** 0.5).to(torch.bfloat16)
+    logits = torch.empty(N, V, device="cuda")
+    lb = torch.empty(N, V, device="cuda", dtype=torch.bfloat16)
+    vals = torch.empty((N, K), dtype=torch.float32, device="cuda")
+    idx = torch.empty((N, K), dtype=torch.int32, device="cuda")
+    runs = {
+        "fused": lambda: osm.proj_softmax_topk(h, w, K, vals, idx),
+        "proj_then_topk": lambda: (osm.proj(h, w, logits), osm.softmax_topk(logits, K, vals, idx)),
+        "proj_only": lambda: osm.proj(h, w, logits),
+        "library_gemm_then_topk": lambda: (torch.matmul(h, w.t(), out=lb),
+                                           osm.softmax_topk(lb, K, vals, idx)),
+    }
+    flops = 2.0 * N * H * V
+    out = {"N": N, "H": H, "V": V, "K": K, "dtype": "bf16 in, f32 accumulate"}
+    for name, fn in runs.items():
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        t = median(timed_calls(fn, reps, stream)) * 1e3
+        out[name + "_us"] = round(t, 1)
+    out["fused_TFLOPs"] = round(flops / out["fused_us"] / 1e6, 1)
+    out["fused_frac_of_mfma_peak"] = round(flops / out["fused_us"] / 1e6 / PEAK_BF16_TFLOPS, 4)
+    out["proj_only_TFLOPs"] = round(flops / out["proj_only_us"] / 1e6, 1)
+    del h, w, logits, lb
+    torch.cuda.empty_cache()
     return out
 
 
@@ -214,6 +251,10 @@ def sweep(path: str):
                   "elements_per_s": round(N * V / us * 1e6, 1), "rows_per_s": round(N / us * 1e6, 1)})
         del x
         torch.cuda.empty_cache()
+    for N, H, V in ((64, 4096, 128256), (512, 4096, 128256), (4000, 1024, 32000),
+                    (4000, 4096, 32000), (4000, 4096, 128256)):
+        rec = proj_compare(osm, torch, N, H, V, 5, 10, stream)
+        emit({"workload": f"proj_{N}x{H}x{V}", "op": "proj_softmax_topk_k5", **rec})
     out.close()
 
 
@@ -341,6 +382,10 @@ def main():
                 "unit": "GB/s", "frac": round(gbs_soft / PEAK_HBM_GBS, 4),
                 "traffic": traffic}
 
+    # projection fused with softmax + top-k (logits never leave the chip)
+    # against the same projection writing logits, then the fused top-k
+    projection = proj_compare(osm, torch, 4000, 1024, 32000, K, args.compare_reps, stream)
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -384,6 +429,7 @@ def main():
         "safe_over_online": round(ratio, 3),
         "online_faster_than_safe_p10_p90_separated": bool(separated),
         "topk_algorithms": algos,
+        "projection_fusion": projection,
         "reference_kernels": reference,
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -193,6 +193,35 @@ OSM_API int softmax_topk_algo(const void* x, void* y, float* vals, int32_t* idx,
 OSM_API int topk_fwd(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
                      int dtype, hipStream_t stream);
 
+/* Largest K of proj_softmax_topk. */
+#define OSM_PROJ_KMAX 16
+
+/* The projection ahead of the softmax in a language model (Section 1):
+ * logits[n][v] = sum_k h[n][k] * w[v][k], on the matrix cores.
+ * h: N*H bfloat16 (hidden vectors, row-major), w: V*H bfloat16 (one row per
+ * vocabulary entry), both 16-byte aligned with H a multiple of 8.
+ * logits: N*V binary32 (binary32 accumulation; the order of the sums is the
+ * kernel's, so results match an exact dot product to within binary32
+ * accumulation error).  logits must not overlap h or w.
+ * Errors: OSM_EINVAL for N < 0, N > 65535 * 128, V < 1, H < 8, H not a
+ * multiple of 8, sizes above 2^31 - 1, null or misaligned pointers. */
+OSM_API int proj_fwd(const void* h, const void* w, float* logits, int64_t N, int64_t H,
+                     int64_t V, hipStream_t stream);
+
+/* The projection fused with the online softmax and top-k (the Discussion's
+ * proposal): for each row n, z = the K indices of the largest logits (Eq. 5,
+ * larger first, equal values in increasing index order) and vals[i] =
+ * softmax(logits[n])[z[i]], without writing the logits anywhere.  Each
+ * 128 x 128 tile of logits is reduced on chip to per-lane online pairs
+ * (Alg. 3) and top-K lists (Alg. 4); partials are merged by Eq. 4 and the key
+ * order.  h, w as in proj_fwd; vals: N*K binary32; idx: N*K int32, 0-based.
+ * Selection is on the binary32 logits as computed by the kernel.
+ * Errors: as proj_fwd, plus OSM_EINVAL for K < 1, K > V, K > OSM_PROJ_KMAX or
+ * overlapping outputs; OSM_ENOMEM if the partials' scratch (N * 4S * (8K + 8)
+ * bytes, S = vocabulary chunks) cannot be allocated. */
+OSM_API int proj_softmax_topk(const void* h, const void* w, float* vals, int32_t* idx,
+                              int64_t N, int64_t H, int64_t V, int K, hipStream_t stream);
+
 /* Kernel family and parameter softmax_fwd would use for this shape on the
  * current device (for OSM_RESIDENT: OSM_KERNEL_ROWS and the threads per row).  Errors: OSM_EINVAL for bad sizes, dtype or
  * null outputs; OSM_EUNSUPPORTED for OSM_RESIDENT rows it cannot hold. */

@@ -20,6 +20,7 @@ RESIDENT_MAX_VEC = 16384
 KERNEL_AUTO, KERNEL_ROWS, KERNEL_SPLIT = 0, 1, 2
 OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM = 0, 1, 2, 3, 4
 TOPK_KMAX = 64
+PROJ_KMAX = 16
 TOPK_ONLINE_FUSED, TOPK_SAFE_FUSED, TOPK_SAFE_UNFUSED, TOPK_ONLINE_UNFUSED, TOPK_VALUES = range(5)
 TOPK_ALGOS = {"online_fused": TOPK_ONLINE_FUSED, "safe_fused": TOPK_SAFE_FUSED,
               "safe_unfused": TOPK_SAFE_UNFUSED, "online_unfused": TOPK_ONLINE_UNFUSED,
@@ -64,6 +65,10 @@ def lib() -> ctypes.CDLL:
     L.topk_fwd.restype = i32
     L.osm_topk_plan.argtypes = [i64, i64, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i64)]
     L.osm_topk_plan.restype = i32
+    L.proj_fwd.argtypes = [vp, vp, vp, i64, i64, i64, vp]
+    L.proj_fwd.restype = i32
+    L.proj_softmax_topk.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, vp]
+    L.proj_softmax_topk.restype = i32
     L.osm_plan.argtypes = [i64, i64, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i64)]
     L.osm_plan.restype = i32
     L.osm_status_string.argtypes = [i32]
@@ -221,3 +226,40 @@ def plan(N: int, V: int, dtype=torch.float32, mode="online"):
     if rc != OK:
         raise OsmError(rc, "osm_plan")
     return k.value, p.value
+
+
+def _proj_inputs(h: torch.Tensor, w: torch.Tensor):
+    for t, nm in ((h, "h"), (w, "w")):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.bfloat16:
+            raise ValueError(f"{nm} must be a bfloat16 CUDA (HIP) tensor")
+        if t.dim() != 2 or not t.is_contiguous():
+            raise ValueError(f"{nm} must be a contiguous 2-D tensor")
+    if h.shape[1] != w.shape[1]:
+        raise ValueError("h (N x H) and w (V x H) must have the same H")
+    return h.shape[0], h.shape[1], w.shape[0]
+
+
+def proj(h: torch.Tensor, w: torch.Tensor, out: torch.Tensor | None = None, stream=None):
+    """logits = h . w^T (``proj_fwd``): h N x H and w V x H bfloat16, binary32 out."""
+    N, H, V = _proj_inputs(h, w)
+    if out is None:
+        out = torch.empty((N, V), dtype=torch.float32, device=h.device)
+    elif (out.dtype != torch.float32 or not out.is_contiguous() or out.numel() != N * V):
+        raise ValueError("out must be a contiguous float32 tensor of N*V elements")
+    rc = lib().proj_fwd(h.data_ptr(), w.data_ptr(), out.data_ptr(), N, H, V, _stream(stream))
+    if rc != OK:
+        raise OsmError(rc, "proj_fwd")
+    return out
+
+
+def proj_softmax_topk(h: torch.Tensor, w: torch.Tensor, K: int, vals: torch.Tensor | None = None,
+                      idx: torch.Tensor | None = None, stream=None):
+    """(vals, idx) = top-k of softmax(h . w^T) per row without writing the
+    logits (``proj_softmax_topk``)."""
+    N, H, V = _proj_inputs(h, w)
+    vals, idx = _topk_outputs(h, N, K, vals, idx)
+    rc = lib().proj_softmax_topk(h.data_ptr(), w.data_ptr(), vals.data_ptr(), idx.data_ptr(),
+                                 N, H, V, int(K), _stream(stream))
+    if rc != OK:
+        raise OsmError(rc, "proj_softmax_topk")
+    return vals, idx

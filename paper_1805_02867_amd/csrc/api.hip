@@ -344,6 +344,61 @@ int run_topk(const void* x, void* y, float* vals, int32_t* idx, int64_t N, int64
     }
 }
 
+// ---------------------------------------------------------------- projection
+constexpr int64_t kProjTile = 128;
+
+// Arguments shared by the projection entry points; OSM_OK if valid.
+int check_proj(const void* h, const void* w, int64_t N, int64_t H, int64_t V) {
+    if (N < 0 || N > 65535 * kProjTile || V < 1 || V > kMaxDim || H < 8 || H > kMaxDim ||
+        H % 8 != 0)
+        return OSM_EINVAL;
+    if (N == 0) return OSM_OK;
+    if (!h || !w || !aligned(h, 16) || !aligned(w, 16)) return OSM_EINVAL;
+    return OSM_OK;
+}
+
+int run_proj_logits(const void* h, const void* w, float* out, int64_t N, int64_t H, int64_t V,
+                    hipStream_t stream) {
+    int st = check_proj(h, w, N, H, V);
+    if (st != OSM_OK || N == 0) return st;
+    if (!out || !aligned(out, 4)) return OSM_EINVAL;
+    const size_t ob = (size_t)N * (size_t)V * 4, hb = (size_t)N * (size_t)H * 2,
+                 wb = (size_t)V * (size_t)H * 2;
+    if (overlaps(out, ob, h, hb) || overlaps(out, ob, w, wb)) return OSM_EINVAL;
+    return hip_status(osm::launch_proj_logits(h, w, out, N, H, V, stream));
+}
+
+int run_proj_topk(const void* h, const void* w, float* vals, int32_t* idx, int64_t N, int64_t H,
+                  int64_t V, int K, hipStream_t stream) {
+    int st = check_proj(h, w, N, H, V);
+    if (st != OSM_OK) return st;
+    if (K < 1 || K > OSM_PROJ_KMAX || (int64_t)K > V) return OSM_EINVAL;
+    if (N == 0) return OSM_OK;
+    if (!vals || !idx || !aligned(vals, 4) || !aligned(idx, 4)) return OSM_EINVAL;
+    const size_t ob = (size_t)N * (size_t)K * 4, hb = (size_t)N * (size_t)H * 2,
+                 wb = (size_t)V * (size_t)H * 2;
+    if (overlaps(vals, ob, idx, ob) || overlaps(vals, ob, h, hb) || overlaps(vals, ob, w, wb) ||
+        overlaps(idx, ob, h, hb) || overlaps(idx, ob, w, wb))
+        return OSM_EINVAL;
+    DeviceState* ds = device_state(nullptr);
+    if (!ds) return OSM_EHIP;
+    // vocabulary chunks: about two workgroups per CU in all
+    const int64_t nb = (N + kProjTile - 1) / kProjTile, nt = (V + kProjTile - 1) / kProjTile;
+    int64_t S = (2 * (int64_t)ds->cus + nb - 1) / nb;
+    if (S > nt) S = nt;
+    if (S < 1) S = 1;
+    const int64_t tiles = (nt + S - 1) / S;
+    S = (nt + tiles - 1) / tiles;
+    void* scratch = nullptr;
+    bool temp = false;
+    st = acquire_scratch(ds, stream, osm::proj_topk_part_bytes(N, S, K), &scratch, &temp);
+    if (st != OSM_OK) return st;
+    hipError_t e = osm::launch_proj_topk(h, w, vals, idx, scratch, N, H, V, K, S, tiles, stream);
+    hipError_t f = temp ? hipFreeAsync(scratch, stream) : hipSuccess;
+    if (e != hipSuccess) return OSM_EHIP;
+    return hip_status(f);
+}
+
 }  // namespace
 
 extern "C" {
@@ -397,6 +452,16 @@ int osm_topk_plan(int64_t N, int64_t V, int dtype, int K, int* kernel, int64_t* 
     *kernel = p.kernel;
     *param = p.param;
     return OSM_OK;
+}
+
+int proj_fwd(const void* h, const void* w, float* logits, int64_t N, int64_t H, int64_t V,
+             hipStream_t stream) {
+    return run_proj_logits(h, w, logits, N, H, V, stream);
+}
+
+int proj_softmax_topk(const void* h, const void* w, float* vals, int32_t* idx, int64_t N,
+                      int64_t H, int64_t V, int K, hipStream_t stream) {
+    return run_proj_topk(h, w, vals, idx, N, H, V, K, stream);
 }
 
 int osm_plan(int64_t N, int64_t V, int dtype, int mode, int* kernel, int64_t* param) {

@@ -22,8 +22,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("softmax_fwd", "softmax_fwd_ex", "softmax_topk", "softmax_topk_dt",
-                 "softmax_topk_ex", "softmax_topk_algo", "topk_fwd", "osm_plan",
-                 "osm_topk_plan", "osm_status_string"):
+                 "softmax_topk_ex", "softmax_topk_algo", "topk_fwd", "proj_fwd",
+                 "proj_softmax_topk", "osm_plan", "osm_topk_plan", "osm_status_string"):
         assert want in names
 
 
@@ -172,6 +172,42 @@ def test_softmax_topk_algo_rejects(args):
 ])
 def test_topk_fwd_rejects(args):
     assert osm.lib().topk_fwd(*args, None) == osm.EINVAL
+
+
+H_, W_, O_ = 0x60000000, 0x70000000, 0x80000000
+
+
+@pytest.mark.parametrize("args", [
+    (H_, W_, O_, -1, 64, 100),           # N < 0
+    (H_, W_, O_, 4, 0, 100),             # H < 8
+    (H_, W_, O_, 4, 60, 100),            # H not a multiple of 8
+    (H_, W_, O_, 4, 64, 0),              # V < 1
+    (H_, W_, O_, 65535 * 128 + 1, 64, 10),  # N above the grid limit
+    (H_ + 2, W_, O_, 4, 64, 100),        # h not 16-byte aligned
+    (H_, W_ + 8, O_, 4, 64, 100),        # w not 16-byte aligned
+    (0, W_, O_, 4, 64, 100),             # null h
+    (H_, W_, 0, 4, 64, 100),             # null output
+    (H_, W_, H_ + 16, 4, 64, 100),       # output overlaps h
+])
+def test_proj_fwd_rejects(args):
+    assert osm.lib().proj_fwd(*args, None) == osm.EINVAL
+
+
+@pytest.mark.parametrize("args", [
+    (H_, W_, V_, I_, 4, 64, 100, 0),     # K < 1
+    (H_, W_, V_, I_, 4, 64, 100, 17),    # K > OSM_PROJ_KMAX
+    (H_, W_, V_, I_, 4, 64, 10, 11),     # K > V
+    (H_, W_, V_, V_ + 4, 4, 64, 100, 5), # idx overlaps vals
+    (H_, W_, W_, I_, 4, 64, 100, 5),     # vals overlaps w
+    (H_, W_, 0, I_, 4, 64, 100, 5),      # null vals
+    (H_, W_, V_, I_, 4, 66, 100, 5),     # H not a multiple of 8
+])
+def test_proj_softmax_topk_rejects(args):
+    assert osm.lib().proj_softmax_topk(*args, None) == osm.EINVAL
+
+
+def test_proj_kmax_matches_header():
+    assert re.search(rf"#define OSM_PROJ_KMAX {osm.PROJ_KMAX}\b", open(HEADER).read())
 
 
 def test_softmax_topk_dt_rejects_unknown_dtype():
