@@ -217,7 +217,7 @@ OSM_API int proj_fwd(const void* h, const void* w, float* logits, int64_t N, int
  * order.  h, w as in proj_fwd; vals: N*K binary32; idx: N*K int32, 0-based.
  * Selection is on the binary32 logits as computed by the kernel.
  * Errors: as proj_fwd, plus OSM_EINVAL for K < 1, K > V, K > OSM_PROJ_KMAX or
- * overlapping outputs; OSM_ENOMEM if the partials' scratch (N * 4S * (8K + 8)
+ * overlapping outputs; OSM_ENOMEM if the partials' scratch (N * 2S * (8K + 8)
  * bytes, S = vocabulary chunks) cannot be allocated. */
 OSM_API int proj_softmax_topk(const void* h, const void* w, float* vals, int32_t* idx,
                               int64_t N, int64_t H, int64_t V, int K, hipStream_t stream);

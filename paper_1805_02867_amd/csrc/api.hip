@@ -349,8 +349,10 @@ constexpr int64_t kProjTile = 128;
 
 // Arguments shared by the projection entry points; OSM_OK if valid.
 int check_proj(const void* h, const void* w, int64_t N, int64_t H, int64_t V) {
+    // the tile grid is one-dimensional: (N / 128) * (V / 128) workgroups < 2^31
     if (N < 0 || N > 65535 * kProjTile || V < 1 || V > kMaxDim || H < 8 || H > kMaxDim ||
-        H % 8 != 0)
+        H % 8 != 0 ||
+        ((N + kProjTile - 1) / kProjTile) * ((V + kProjTile - 1) / kProjTile) > (kMaxDim - 7))
         return OSM_EINVAL;
     if (N == 0) return OSM_OK;
     if (!h || !w || !aligned(h, 16) || !aligned(w, 16)) return OSM_EINVAL;
