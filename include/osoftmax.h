@@ -203,8 +203,9 @@ OSM_API int topk_fwd(const void* x, float* vals, int32_t* idx, int64_t N, int64_
  * logits: N*V binary32 (binary32 accumulation; the order of the sums is the
  * kernel's, so results match an exact dot product to within binary32
  * accumulation error).  logits must not overlap h or w.
- * Errors: OSM_EINVAL for N < 0, N > 65535 * 128, V < 1, H < 8, H not a
- * multiple of 8, sizes above 2^31 - 1, null or misaligned pointers. */
+ * Errors: OSM_EINVAL for N < 0, N > 65535 * 128, V < 1, H < 8, H > 2^20,
+ * H not a multiple of 8, sizes above 2^31 - 1, null or misaligned
+ * pointers. */
 OSM_API int proj_fwd(const void* h, const void* w, float* logits, int64_t N, int64_t H,
                      int64_t V, hipStream_t stream);
 
@@ -212,7 +213,7 @@ OSM_API int proj_fwd(const void* h, const void* w, float* logits, int64_t N, int
  * proposal): for each row n, z = the K indices of the largest logits (Eq. 5,
  * larger first, equal values in increasing index order) and vals[i] =
  * softmax(logits[n])[z[i]], without writing the logits anywhere.  Each
- * 128 x 128 tile of logits is reduced on chip to per-lane online pairs
+ * 256 x 256 tile of logits is reduced on chip to per-lane online pairs
  * (Alg. 3) and top-K lists (Alg. 4); partials are merged by Eq. 4 and the key
  * order.  h, w as in proj_fwd; vals: N*K binary32; idx: N*K int32, 0-based.
  * Selection is on the binary32 logits as computed by the kernel.

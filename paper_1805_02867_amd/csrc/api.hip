@@ -345,12 +345,13 @@ int run_topk(const void* x, void* y, float* vals, int32_t* idx, int64_t N, int64
 }
 
 // ---------------------------------------------------------------- projection
-constexpr int64_t kProjTile = 128;
+constexpr int64_t kProjTile = 128;     // smallest tile edge of the projection kernels
+constexpr int64_t kProjMaxH = 1 << 20;  // 32-bit load offsets within a tile
 
 // Arguments shared by the projection entry points; OSM_OK if valid.
 int check_proj(const void* h, const void* w, int64_t N, int64_t H, int64_t V) {
     // the tile grid is one-dimensional: (N / 128) * (V / 128) workgroups < 2^31
-    if (N < 0 || N > 65535 * kProjTile || V < 1 || V > kMaxDim || H < 8 || H > kMaxDim ||
+    if (N < 0 || N > 65535 * kProjTile || V < 1 || V > kMaxDim || H < 8 || H > kProjMaxH ||
         H % 8 != 0 ||
         ((N + kProjTile - 1) / kProjTile) * ((V + kProjTile - 1) / kProjTile) > (kMaxDim - 7))
         return OSM_EINVAL;
@@ -367,7 +368,9 @@ int run_proj_logits(const void* h, const void* w, float* out, int64_t N, int64_t
     const size_t ob = (size_t)N * (size_t)V * 4, hb = (size_t)N * (size_t)H * 2,
                  wb = (size_t)V * (size_t)H * 2;
     if (overlaps(out, ob, h, hb) || overlaps(out, ob, w, wb)) return OSM_EINVAL;
-    return hip_status(osm::launch_proj_logits(h, w, out, N, H, V, stream));
+    DeviceState* ds = device_state(nullptr);
+    if (!ds) return OSM_EHIP;
+    return hip_status(osm::launch_proj_logits(h, w, out, N, H, V, ds->cus, stream));
 }
 
 int run_proj_topk(const void* h, const void* w, float* vals, int32_t* idx, int64_t N, int64_t H,
@@ -384,18 +387,15 @@ int run_proj_topk(const void* h, const void* w, float* vals, int32_t* idx, int64
         return OSM_EINVAL;
     DeviceState* ds = device_state(nullptr);
     if (!ds) return OSM_EHIP;
-    // vocabulary chunks: about two workgroups per CU in all
-    const int64_t nb = (N + kProjTile - 1) / kProjTile, nt = (V + kProjTile - 1) / kProjTile;
-    int64_t S = (2 * (int64_t)ds->cus + nb - 1) / nb;
-    if (S > nt) S = nt;
-    if (S < 1) S = 1;
-    const int64_t tiles = (nt + S - 1) / S;
-    S = (nt + tiles - 1) / tiles;
+    int64_t S = 1, tiles = 1;
+    int parts = 2;
+    osm::proj_topk_shape(N, V, K, ds->cus, &S, &tiles, &parts);
     void* scratch = nullptr;
     bool temp = false;
-    st = acquire_scratch(ds, stream, osm::proj_topk_part_bytes(N, S, K), &scratch, &temp);
+    st = acquire_scratch(ds, stream, osm::proj_topk_part_bytes(N, S, parts, K), &scratch, &temp);
     if (st != OSM_OK) return st;
-    hipError_t e = osm::launch_proj_topk(h, w, vals, idx, scratch, N, H, V, K, S, tiles, stream);
+    hipError_t e =
+        osm::launch_proj_topk(h, w, vals, idx, scratch, N, H, V, K, S, tiles, parts, stream);
     hipError_t f = temp ? hipFreeAsync(scratch, stream) : hipSuccess;
     if (e != hipSuccess) return OSM_EHIP;
     return hip_status(f);

@@ -24,17 +24,21 @@ hipError_t launch_softmax_split(const void* x, void* y, void* scratch, int64_t N
 hipError_t launch_softmax_resident(const void* x, void* y, int64_t N, int64_t V, int dtype,
                                    int block, int r, bool vec, hipStream_t st);
 
-// Projection (bfloat16 h: N x H, w: V x H, H a multiple of 8, 16-byte
-// aligned): logits = h . w^T in binary32.
+// Projection (bfloat16 h: N x H, w: V x H, H a multiple of 8 and at most
+// 2^20, 16-byte aligned): logits = h . w^T in binary32; cus = compute units.
 hipError_t launch_proj_logits(const void* h, const void* w, float* out, int64_t N, int64_t H,
-                              int64_t V, hipStream_t st);
+                              int64_t V, int cus, hipStream_t st);
 
 // Projection fused with the online softmax and top-k: S vocabulary chunks of
-// `tiles` 128-entry tiles; part holds proj_topk_part_bytes(N, S, K) bytes.
-size_t proj_topk_part_bytes(int64_t N, int64_t S, int K);
+// `tiles` tiles each, `parts` partials per (row, chunk) (proj_topk_shape
+// picks all three for a device with `cus` compute units); part holds
+// proj_topk_part_bytes(N, S, parts, K) bytes.
+void proj_topk_shape(int64_t N, int64_t V, int K, int cus, int64_t* S, int64_t* tiles,
+                     int* parts);
+size_t proj_topk_part_bytes(int64_t N, int64_t S, int parts, int K);
 hipError_t launch_proj_topk(const void* h, const void* w, float* vals, int32_t* idx,
                             void* part, int64_t N, int64_t H, int64_t V, int K, int64_t S,
-                            int64_t tiles, hipStream_t st);
+                            int64_t tiles, int parts, hipStream_t st);
 
 // What the top-k kernels compute next to the selection (Section 4, and the
 // comparisons of Section 5.2):

@@ -3,10 +3,15 @@
 // ahead of the softmax (Section 1) is logits = h . W^T; the Discussion's
 // fusion runs the softmax (+ top-k) on the tile while it is still on chip.
 //
-// Tile: 128 x 128 of P per workgroup of 256 threads (four wavefronts, each
-// 64 x 64 = 2 x 2 blocks of v_mfma_f32_32x32x16_bf16).  K advances in steps
-// of 64 through two pairs of LDS tiles filled by direct-to-LDS loads (no
-// staging registers); one barrier per step.
+// Tile: TX x TY of P per workgroup of WX x WY wavefronts, each a block of
+// 32 x 32 v_mfma_f32_32x32x16_bf16 products.  K advances in steps of 64
+// through two LDS stages.  Operands travel global -> LDS by buffer loads
+// with the LDS as destination (no staging registers); the buffer descriptor
+// of each operand starts at the tile's first row and ends at the matrix's
+// end, so rows past the matrix, and chunks past K (given an offset beyond
+// the descriptor), read as zeros without any branch on the load path.  The
+// step count is rounded up to even, the extra step reading zeros, so that
+// every tile starts in stage 0 and both stages have fixed roles in the code.
 //
 // MFMA 32x32x16 lane layout (checked on the hardware): lane l supplies
 // A[m = l % 32][k = 8 (l / 32) + j] and B[k = 8 (l / 32) + j][n = l % 32] for
@@ -21,80 +26,112 @@ namespace osm {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int PJ_BLOCK = 256;
-constexpr int PJ_TX = 128;               // tile rows of P taken from X
-constexpr int PJ_TY = 128;               // tile columns of P taken from Y
-constexpr int PJ_BK = 64;                // K per step
-constexpr int PJ_CHUNKS = PJ_TX * PJ_BK / 8 / PJ_BLOCK;  // 16-byte loads per thread per tile
-
-// LDS: the X and Y tiles of two K steps, 128 rows of 64 bfloat16 (128 B)
-// each.  Within a row, 16-byte chunk kc sits in slot kc ^ (row & 7), so the
-// eight lanes of each phase of a fragment read (eight consecutive rows, one
-// chunk) hit eight different slots, i.e. distinct banks.
-struct ProjSmem {
-    uint16_t x0[PJ_TX][PJ_BK];
-    uint16_t y0[PJ_TY][PJ_BK];
-    uint16_t x1[PJ_TX][PJ_BK];
-    uint16_t y1[PJ_TY][PJ_BK];
-};
+constexpr int PJ_BK = 64;  // K per step
 
 // Workgroups are dealt to the eight XCDs in turn (workgroup b to XCD b % 8),
 // each with its own L2.  Logical id of workgroup b when XCD k takes the k-th
 // contiguous block of `per` logical ids, so that the workgroups sharing an
 // L2 work on neighbouring tiles and share their operand tiles there.  The
-// grid holds 8 * per workgroups; ids past `total` have no work.
+// grid holds 8 * per workgroups; ids past the tile count have no work.
 __device__ __forceinline__ int64_t xcd_logical(int64_t b, int64_t per) {
     return (b % 8) * per + b / 8;
 }
 
-// Row `r`, result register `i` of a wavefront's 64 x 64 block: the P row
-// within the block is 32 mi + row_in_32(i, lane), the column 32 ni + lane % 32.
+// P row of result register `i` within a 32 x 32 block: 8 (i / 4) + 4 (l / 32) + i % 4.
 __device__ __forceinline__ int row_in_32(int i, int lane) {
     return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
 }
 
-// 16 zero bytes in device memory: the source of every chunk that lies outside
-// a matrix (the direct-to-LDS load cannot be zeroed after it lands).
-__device__ const u32x4 pj_zero16 = {0u, 0u, 0u, 0u};
+// LDS slot of 16-byte chunk kc of a tile row (rows of 64 bfloat16, 128 B).
+// The LDS serves a 16-byte-per-lane read 16 lanes at a time from 64
+// four-byte banks (256 B); the 16 lanes of a fragment read hold 16
+// consecutive rows and one chunk, two rows per 256 B of banks, so the slot
+// is XORed with (row / 2) % 8: the 16 (row parity, slot) pairs are then all
+// distinct and the read is free of bank conflicts.
+__device__ __forceinline__ int pj_slot(int row, int kc) { return kc ^ ((row >> 1) & 7); }
 
-// Global -> LDS without registers: the 128 x 64 tile of a row-major matrix
-// (`rows` x K, K a multiple of 8) at (r0, k0) into `tile`.  Each wavefront
-// issues four 16-byte-per-lane direct-to-LDS loads; lane l of load j lands in
-// LDS chunk p = 64 (4 j + wave) + l, i.e. row p / 8, slot p % 8, which holds
-// the row's chunk (p % 8) ^ (row & 7).
-__device__ __forceinline__ void pj_dma(uint16_t (&tile)[PJ_TX][PJ_BK],
-                                       const uint16_t* __restrict__ m, int64_t rows, int64_t K,
-                                       int64_t r0, int64_t k0) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+template <int TX_, int TY_, int WX_, int WY_>
+struct PjCfg {
+    static constexpr int TX = TX_, TY = TY_, WX = WX_, WY = WY_;
+    static constexpr int NW = WX * WY, NT = 64 * NW;            // wavefronts, threads
+    static constexpr int MI = TX / 32 / WX, NI = TY / 32 / WY;  // blocks per wavefront
+    static constexpr int LX = TX * 8 / NT, LY = TY * 8 / NT;    // loads per thread per stage
+    static_assert(LX * NT == TX * 8 && LY * NT == TY * 8, "whole loads");
+    // X and Y tiles of the two stages (each stage contiguous)
+    struct Stage {
+        uint16_t x[TX][PJ_BK];
+        uint16_t y[TY][PJ_BK];
+    };
+    struct Smem {
+        Stage st[2];
+    };
+};
+
+// Buffer descriptor of `m` (rows x K) from row r0 on; reads at byte offsets
+// at or past its size return zeros.  Valid offsets in a tile stay below
+// 256 K 2 <= 2^29 (K <= 2^20), so the size saturates at 2^31 - 1 harmlessly.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t pj_rsrc(const uint16_t* m, int64_t rows,
+                                                         int64_t K, int64_t r0) {
+    const int64_t bytes = (rows - r0) * K * 2;
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(m + r0 * K), (short)0,
+                                             (int)(bytes < 0x7FFFFFFF ? bytes : 0x7FFFFFFF),
+                                             0x00020000);
+}
+constexpr uint32_t PJ_OOB = 0x80000000u;  // an offset past every descriptor
+
+// Per-thread part of the load addressing: load j of a stage covers LDS chunk
+// p = 64 (NW j + wave) + lane, i.e. row p / 8, slot p % 8, which holds the
+// row's chunk kc = pj_slot(row, p % 8) (the map is an involution).  Row
+// p / 8 = 8 (NW j + wave) + lane / 8, so kc does not depend on j, and the
+// byte offset of load j is voff + j * jstride.
+struct PjAddr {
+    uint32_t voff, jstride;
+    int kc;
+    template <class C>
+    __device__ __forceinline__ static PjAddr make(int64_t K) {
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+        const int p = 64 * wave + lane;
+        const int row = p >> 3, kc = pj_slot(row, p & 7);
+        return PjAddr{(uint32_t)(row * K * 2 + kc * 16), (uint32_t)(8 * C::NW * K * 2), kc};
+    }
+};
+
+// Loads of step k (elements 64 k ... of each row) of one operand tile.
+// Wavefront index, known to the compiler to be uniform (scalar registers).
+__device__ __forceinline__ int pj_wave() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
+template <class C, int ROWS, int L>
+__device__ __forceinline__ void pj_dma(uint16_t (&tile)[ROWS][PJ_BK], __amdgpu_buffer_rsrc_t rs,
+                                       const PjAddr& a, int64_t K, int64_t k) {
+    const int wave = pj_wave();
+    const int64_t k0 = k * PJ_BK;
+    // chunks at or past K (the last step of a ragged K, and padded steps) read zeros
+    const bool oob = k0 + PJ_BK > K && k0 + a.kc * 8 >= K;
 #pragma unroll
-    for (int j = 0; j < PJ_CHUNKS; ++j) {
-        const int base = 64 * (4 * j + wave);  // first chunk of this load (wave-uniform)
-        const int p = base + lane;
-        const int row = p >> 3, kc = (p & 7) ^ (row & 7);
-        const int64_t grow = r0 + row, gcol = k0 + kc * 8;
-        const void* src = (grow < rows && gcol < K) ? (const void*)(m + grow * K + gcol)
-                                                   : (const void*)&pj_zero16;
-        __builtin_amdgcn_global_load_lds(
-            (const void __attribute__((address_space(1)))*)src,
-            (__attribute__((address_space(3))) void*)(&tile[0][0] + base * 8), 16, 0, 0);
+    for (int j = 0; j < L; ++j) {
+        const int base = 64 * (C::NW * j + wave);  // first chunk of this load (wave-uniform)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rs, (__attribute__((address_space(3))) void*)(&tile[0][0] + base * 8), 16,
+            oob ? PJ_OOB : a.voff + j * a.jstride, (int)(k0 * 2), 0, 0);
     }
 }
 
 // The 16-byte fragment of row r, chunk kc of a tile.
-__device__ __forceinline__ bf16x8 pj_frag(const uint16_t (&tile)[PJ_TX][PJ_BK], int r, int kc) {
+template <int ROWS>
+__device__ __forceinline__ bf16x8 pj_frag(const uint16_t (&tile)[ROWS][PJ_BK], int r, int kc) {
     return __builtin_bit_cast(
-        bf16x8, *reinterpret_cast<const u32x4*>(&tile[r][((kc ^ (r & 7)) * 8)]));
+        bf16x8, *reinterpret_cast<const u32x4*>(&tile[r][pj_slot(r, kc) * 8]));
 }
 
 // acc[mi][ni] += the wavefront's (32 MI) x (32 NI) block of X-tile . Y-tile^T
 // over one K step; the block starts at row bx of the X tile and row by of the
 // Y tile.  The fragments of sub-step ks + 1 are read into the other register
-// set before the products of sub-step ks are issued, so the LDS latency is
-// exposed once per step rather than before every group of products.
-template <int MI, int NI>
-__device__ __forceinline__ void pj_mma(const uint16_t (&xt)[PJ_TX][PJ_BK],
-                                       const uint16_t (&yt)[PJ_TY][PJ_BK], int bx, int by,
-                                       f32x16 (&acc)[MI][NI]) {
+// set before the products of sub-step ks are issued.
+template <class C>
+__device__ __forceinline__ void pj_mma(const uint16_t (&xt)[C::TX][PJ_BK],
+                                       const uint16_t (&yt)[C::TY][PJ_BK], int bx, int by,
+                                       f32x16 (&acc)[C::MI][C::NI]) {
+    constexpr int MI = C::MI, NI = C::NI, KS = PJ_BK / 16;
     const int lane = threadIdx.x & 63;
     const int lr = lane & 31, lh = lane >> 5;
     bf16x8 a[2][MI], b[2][NI];  // [register set][block]
@@ -106,9 +143,9 @@ __device__ __forceinline__ void pj_mma(const uint16_t (&xt)[PJ_TX][PJ_BK],
     };
     read(0, 0);
 #pragma unroll
-    for (int ks = 0; ks < PJ_BK / 16; ++ks) {
+    for (int ks = 0; ks < KS; ++ks) {
         const int cur = ks & 1;
-        if (ks + 1 < PJ_BK / 16) read(cur ^ 1, ks + 1);
+        if (ks + 1 < KS) read(cur ^ 1, ks + 1);
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
@@ -121,59 +158,86 @@ __device__ __forceinline__ void pj_mma(const uint16_t (&xt)[PJ_TX][PJ_BK],
     // LDS reads, 0x008: matrix instructions).
     __builtin_amdgcn_sched_group_barrier(0x100, MI + NI, 0);
 #pragma unroll
-    for (int ks = 0; ks < PJ_BK / 16; ++ks) {
-        if (ks + 1 < PJ_BK / 16) __builtin_amdgcn_sched_group_barrier(0x100, MI + NI, 0);
+    for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x100, MI + NI, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, MI * NI, 0);
     }
 }
 
-// The workgroup's 128 x 128 tile of P at (x0, y0), accumulated over all of K,
-// by WX x WY wavefronts (WX WY = 4), each a (128 / WX) x (128 / WY) block:
-// wavefront w covers X rows 32 MI (w / WY) and Y rows 32 NI (w % WY) on.
-// Every thread of the workgroup must call it (it synchronises).  The next
-// step's tiles stream straight into the other pair of LDS buffers while the
-// current pair is multiplied; the loop is unrolled by two so that each
-// buffer's role is fixed in the code (the compiler then knows the loads in
-// flight do not alias the tiles being read, and waits for them only before
-// the step's barrier).
-template <int WX, int WY>
-__device__ __forceinline__ void pj_tile(const uint16_t* __restrict__ X, int64_t nx,
-                                        const uint16_t* __restrict__ Y, int64_t ny, int64_t K,
-                                        int64_t x0, int64_t y0, ProjSmem& sm,
-                                        f32x16 (&acc)[PJ_TX / 32 / WX][PJ_TY / 32 / WY]) {
-    static_assert(WX * WY == PJ_BLOCK / 64, "one block per wavefront");
-    constexpr int MI = PJ_TX / 32 / WX, NI = PJ_TY / 32 / WY;
-    const int wave = threadIdx.x >> 6;
-    const int bx = (wave / WY) * 32 * MI, by = (wave % WY) * 32 * NI;
+// Stage hand-over.  The loads of the next stage were issued one step
+// earlier; each thread waits for its own, then the workgroup barrier makes
+// every thread's loads visible and tells that every wavefront has finished
+// reading the stage about to be refilled.  (A plain s_barrier: the fenced
+// __syncthreads would also make the compiler wait for everything else.)
+__device__ __forceinline__ void pj_handover() {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Step count of a K: whole steps of 64, rounded up to even.
+__device__ __forceinline__ int64_t pj_steps(int64_t K) {
+    return ((K + PJ_BK - 1) / PJ_BK + 1) / 2 * 2;
+}
+
+// Issue both operands' loads of step k into stage `st`.
+template <class C>
+__device__ __forceinline__ void pj_issue(typename C::Smem& sm, int st, __amdgpu_buffer_rsrc_t rx,
+                                         __amdgpu_buffer_rsrc_t ry, const PjAddr& a, int64_t K,
+                                         int64_t k) {
+    pj_dma<C, C::TX, C::LX>(sm.st[st].x, rx, a, K, k);
+    pj_dma<C, C::TY, C::LY>(sm.st[st].y, ry, a, K, k);
+}
+
+// The workgroup's tiles t = t0, t0 + 1, ... < t1, each TX x TY of P at
+// coords(t) = (x0, y0) (x0 < nx, y0 < ny), accumulated over all of K;
+// epi(t, x0, y0, acc) runs after each tile with stage 1 of the LDS free for
+// its own use (every wavefront is past its last read of it, and it is
+// refilled only after the next tile's first hand-over).  The next tile's
+// first stage is in flight while epi runs.  Every thread of the workgroup
+// must call this, with t0 < t1.
+template <class C, class Coords, class Epi>
+__device__ __forceinline__ void pj_run(const uint16_t* __restrict__ X, int64_t nx,
+                                       const uint16_t* __restrict__ Y, int64_t ny, int64_t K,
+                                       int64_t t0, int64_t t1, typename C::Smem& sm,
+                                       Coords&& coords, Epi&& epi) {
+    const int wave = pj_wave();
+    const int bx = (wave / C::WY) * 32 * C::MI, by = (wave % C::WY) * 32 * C::NI;
+    const PjAddr a = PjAddr::make<C>(K);
+    const int64_t nk = pj_steps(K);
+    int64_t x0, y0;
+    coords(t0, x0, y0);
+    __amdgpu_buffer_rsrc_t rx = pj_rsrc(X, nx, K, x0), ry = pj_rsrc(Y, ny, K, y0);
+    pj_issue<C>(sm, 0, rx, ry, a, K, 0);
+    for (int64_t t = t0; t < t1; ++t) {
+        const bool more = t + 1 < t1;
+        int64_t xn = x0, yn = y0;
+        if (more) coords(t + 1, xn, yn);
+        const __amdgpu_buffer_rsrc_t rxn = pj_rsrc(X, nx, K, xn), ryn = pj_rsrc(Y, ny, K, yn);
+        f32x16 acc[C::MI][C::NI];
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
+        for (int mi = 0; mi < C::MI; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < NI; ++ni)
+            for (int ni = 0; ni < C::NI; ++ni)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.0f;
-    const int64_t nk = (K + PJ_BK - 1) / PJ_BK;
-    __syncthreads();  // the previous tile's readers of the buffers are done
-    pj_dma(sm.x0, X, nx, K, x0, 0);
-    pj_dma(sm.y0, Y, ny, K, y0, 0);
-    __syncthreads();
-    int64_t kb = 0;
-    for (; kb + 2 <= nk; kb += 2) {
-        if (kb + 1 < nk) {
-            pj_dma(sm.x1, X, nx, K, x0, (kb + 1) * PJ_BK);
-            pj_dma(sm.y1, Y, ny, K, y0, (kb + 1) * PJ_BK);
+                for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.0f;
+        for (int64_t k = 0; k < nk; k += 2) {
+            pj_handover();
+            pj_issue<C>(sm, 1, rx, ry, a, K, k + 1);
+            pj_mma<C>(sm.st[0].x, sm.st[0].y, bx, by, acc);
+            pj_handover();
+            if (k + 2 < nk) pj_issue<C>(sm, 0, rx, ry, a, K, k + 2);
+            else if (more) pj_issue<C>(sm, 0, rxn, ryn, a, K, 0);
+            pj_mma<C>(sm.st[1].x, sm.st[1].y, bx, by, acc);
         }
-        pj_mma<MI, NI>(sm.x0, sm.y0, bx, by, acc);
-        __syncthreads();
-        if (kb + 2 < nk) {
-            pj_dma(sm.x0, X, nx, K, x0, (kb + 2) * PJ_BK);
-            pj_dma(sm.y0, Y, ny, K, y0, (kb + 2) * PJ_BK);
-        }
-        pj_mma<MI, NI>(sm.x1, sm.y1, bx, by, acc);
-        __syncthreads();
-    }
-    if (kb < nk) {
-        pj_mma<MI, NI>(sm.x0, sm.y0, bx, by, acc);
-        __syncthreads();
+        // every wavefront's last read of stage 1 is done before epi may write it
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        epi(t, x0, y0, acc);
+        x0 = xn;
+        y0 = yn;
+        rx = rxn;
+        ry = ryn;
     }
 }
 

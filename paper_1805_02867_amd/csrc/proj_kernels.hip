@@ -3,9 +3,10 @@
 // that the logits never leave the chip (the Discussion's proposal).
 //
 // Fused kernel.  Workgroup (c, b) computes P = W . h^T for the vocabulary
-// tiles of chunk c against batch rows [128 b, 128 b + 128): with W as the
-// MFMA's A operand, each lane's result registers hold 64 vocabulary entries
-// of one batch row (a column of P) per tile, so a lane keeps, for that row,
+// tiles of chunk c against batch rows [256 b, 256 b + 256): with W as the
+// MFMA's A operand, each lane's result registers hold, per tile, 128
+// vocabulary entries of each of two batch rows (columns of P), so a lane
+// keeps, for each of those rows,
 //  * the online pair (s, d) of the entries it has seen (Alg. 3's update,
 //    with the reference moved only when the tile maximum passes it by more
 //    than kLazy, as in the other one-pass kernels), and
@@ -20,43 +21,68 @@
 
 namespace osm {
 
+// Plain logits: 256 x 256 tiles for eight wavefronts when the tile count
+// fills the chip twice over, else 128 x 128 tiles for four (two workgroups
+// per CU), which keep small problems spread over more CUs.
+using PjBig = PjCfg<256, 256, 2, 4>;
+using PjSmall = PjCfg<128, 128, 2, 2>;
+// Fused, by batch size and K (the vocabulary tile is 256 entries in all):
+//  * 256 x 256 (K <= 8, N > 128): four wavefronts side by side along the
+//    batch, two batch rows per lane, the lanes' top-K lists in the 32 KB of
+//    LDS beside the two stages (the core takes the registers);
+//  * 256 x 128 (otherwise, N > 64): one batch row per lane, lists in
+//    registers;
+//  * 256 x 64 (N <= 64): 2 x 2 wavefronts, one batch row per lane, so small
+//    batches do not pay for a strip of 256 rows.
+using PjFused8 = PjCfg<256, 256, 1, 4>;
+using PjFused16 = PjCfg<256, 128, 1, 4>;
+using PjFusedN = PjCfg<256, 64, 2, 2>;
+static int fused_cfg(int64_t N, int K) { return N <= 64 ? 2 : (K <= 8 && N > 128 ? 0 : 1); }
+
 // ------------------------------------------------------------ plain logits
 // Tiles in grouped order: groups of up to 8 batch strips, each taken across
 // all vocabulary tiles before the next group, so that a contiguous block of
 // logical ids covers a compact block of tiles.
 constexpr int64_t PJ_GROUP = 8;
 
-__global__ __launch_bounds__(PJ_BLOCK) void proj_logits(const uint16_t* __restrict__ h,
-                                                       const uint16_t* __restrict__ w,
-                                                       float* __restrict__ out, int64_t N,
-                                                       int64_t H, int64_t V, int64_t per) {
-    __shared__ ProjSmem sm;
-    const int64_t nb = (N + PJ_TX - 1) / PJ_TX, nt = (V + PJ_TY - 1) / PJ_TY;
-    const int64_t L = xcd_logical(blockIdx.x, per);
-    if (L >= nb * nt) return;  // the whole workgroup leaves
+template <class C>
+__global__ __launch_bounds__(C::NT) void proj_logits(const uint16_t* __restrict__ h,
+                                                     const uint16_t* __restrict__ w,
+                                                     float* __restrict__ out, int64_t N,
+                                                     int64_t H, int64_t V, int64_t per) {
+    __shared__ typename C::Smem sm;
+    const int64_t nb = (N + C::TX - 1) / C::TX, nt = (V + C::TY - 1) / C::TY;
+    const int64_t lid = xcd_logical(blockIdx.x, per);
+    if (lid >= nb * nt) return;  // the whole workgroup leaves
     const int64_t in_group = PJ_GROUP * nt;
-    const int64_t first = (L / in_group) * PJ_GROUP;
+    const int64_t first = (lid / in_group) * PJ_GROUP;
     const int64_t gsize = nb - first < PJ_GROUP ? nb - first : PJ_GROUP;
-    const int64_t x0 = (first + (L % in_group) % gsize) * PJ_TX;  // batch
-    const int64_t y0 = ((L % in_group) / gsize) * PJ_TY;          // vocabulary
-    f32x16 acc[2][2];
-    pj_tile<2, 2>(h, N, w, V, H, x0, y0, sm, acc);
+    const int64_t bx0 = (first + (lid % in_group) % gsize) * C::TX;  // batch
+    const int64_t vy0 = ((lid % in_group) / gsize) * C::TY;          // vocabulary
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wx = wave >> 1, wy = wave & 1;
+    const int wx = wave / C::WY, wy = wave % C::WY;
+    pj_run<C>(
+        h, N, w, V, H, 0, 1, sm,
+        [&](int64_t, int64_t& x0, int64_t& y0) {
+            x0 = bx0;
+            y0 = vy0;
+        },
+        [&](int64_t, int64_t x0, int64_t y0, f32x16 (&acc)[C::MI][C::NI]) {
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+            for (int mi = 0; mi < C::MI; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
+                for (int ni = 0; ni < C::NI; ++ni)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int64_t row = x0 + wx * 64 + mi * 32 + row_in_32(i, lane);
-                const int64_t col = y0 + wy * 64 + ni * 32 + (lane & 31);
-                if (row < N && col < V) out[row * V + col] = acc[mi][ni][i];
-            }
+                    for (int i = 0; i < 16; ++i) {
+                        const int64_t row = x0 + wx * 32 * C::MI + mi * 32 + row_in_32(i, lane);
+                        const int64_t col = y0 + wy * 32 * C::NI + ni * 32 + (lane & 31);
+                        if (row < N && col < V) out[row * V + col] = acc[mi][ni][i];
+                    }
+        });
 }
 
 // ------------------------------------------------------------ fused top-k
-// Insert `key` into the lane's list (descending, K valid entries in a
+// Insert `key` into a lane's list (descending, K valid entries in a
 // register array of KC, unused entries 0); the caller has checked that key
 // exceeds the K-th entry.  Every entry moves at most one place, computed
 // from the old list, so all positions update at once.
@@ -81,145 +107,363 @@ __device__ __forceinline__ uint64_t list_kth(const uint64_t (&L)[KC], int K) {
     return t;
 }
 
-// One chunk of the vocabulary for one 128-row batch strip.  The four
-// wavefronts sit side by side along the batch (each 128 vocabulary entries x
-// 32 batch rows, 4 x 1 blocks), so lane l of wavefront w holds, for batch row
-// 32 w + l % 32 of the strip, 64 vocabulary entries of each tile: the entries
-// 32 mi + row_in_32(i, l) for result register i of block mi.  The two lane
-// halves of a batch row each write a partial: 2 S per row (chunk, half), each
-// a pair and K keys (0 = none).
+// A copy of an accumulator register made where it is used.  Left to itself
+// the compiler moves every accumulator of the tile into vector registers at
+// once when the products end (they are read by vector instructions from
+// then on), which overflows the register file; reading each one through
+// this keeps the accumulators where the products left them.
+__device__ __forceinline__ float acc_reread(float a) {
+    float r;
+    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(r) : "a"(a));
+    return r;
+}
+
+// Bit j of a candidate mask for entry x against threshold t, set when x is
+// below t: the sign of x - t, moved to bit j in vector registers (a compare
+// would give a wave-wide scalar mask per entry, and the compiler keeps many
+// of those alive at once).  x == t gives +0, i.e. not below; a NaN
+// difference may set either value, and every candidate is checked again
+// before it is offered.
+__device__ __forceinline__ uint32_t below_bit(float x, float t, int j) {
+    return (__float_as_uint(x - t) >> 31) << j;
+}
+
+// A lane's top-K list (descending keys, K valid, unused entries 0): KC
+// registers, or KC words of LDS (thread t's entry i at word i * NT + t).
+template <int KC, bool LDS>
+struct LaneList;
 template <int KC>
-__global__ __launch_bounds__(PJ_BLOCK) __attribute__((amdgpu_waves_per_eu(2, 2))) void proj_topk_part(
+struct LaneList<KC, false> {
+    uint64_t L[KC];
+    __device__ __forceinline__ void init(uint64_t*) {
+#pragma unroll
+        for (int i = 0; i < KC; ++i) L[i] = 0ull;
+    }
+    // insert (key > K-th entry); returns the new K-th entry
+    __device__ __forceinline__ uint64_t insert(uint64_t*, int K, uint64_t key) {
+        list_insert<KC>(L, K, key);
+        return list_kth<KC>(L, K);
+    }
+    __device__ __forceinline__ uint64_t get(const uint64_t*, int i) const { return L[i]; }
+};
+template <int KC>
+struct LaneList<KC, true> {
+    static constexpr int NT = 256;  // threads of the workgroup (the column stride)
+    __device__ __forceinline__ void init(uint64_t* m) {
+#pragma unroll
+        for (int i = 0; i < KC; ++i) m[i * NT] = 0ull;
+    }
+    __device__ __forceinline__ uint64_t insert(uint64_t* m, int K, uint64_t key) {
+        uint64_t L[KC];
+#pragma unroll
+        for (int i = 0; i < KC; ++i) L[i] = m[i * NT];
+        list_insert<KC>(L, K, key);
+#pragma unroll
+        for (int i = 0; i < KC; ++i) m[i * NT] = L[i];
+        return list_kth<KC>(L, K);
+    }
+    __device__ __forceinline__ uint64_t get(const uint64_t* m, int i) const { return m[i * NT]; }
+};
+
+// One chunk of vocabulary tiles [c * tiles, min((c + 1) * tiles, nt)) for one
+// batch strip of TY rows.  Lane l of wavefront w holds, for batch rows
+// (TY / 4) w + 32 ni + l % 32 (ni < NI) of the strip, the entries
+// vbase + 32 mi + 8 (i / 4) + i % 4 (vbase = tile start + 4 (l / 32), mi < 8)
+// in result register i of block (mi, ni).  The partial of a (row, chunk) pair
+// written by this lane is p = 2 c + l / 32: 2 S per row, each a pair and K
+// keys (0 = none).
+template <class C, int KC, bool LDSL>
+__global__ __launch_bounds__(C::NT) void proj_topk_part(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, uint64_t* __restrict__ pkeys,
     MD* __restrict__ pmd, int64_t N, int64_t H, int64_t V, int K, int64_t S, int64_t tiles,
     int64_t per) {
-    __shared__ ProjSmem sm;
-    static_assert(sizeof(ProjSmem) >= PJ_BLOCK * 64 * sizeof(float), "epilogue scratch fits");
+    static_assert(!LDSL || C::NT == 256, "LDS lists are laid out for 256 threads");
+    constexpr int NI = C::NI;
+    constexpr int E = C::MI * 16;  // entries per row per lane and tile
+    // entries per pass of the LDS column: the largest power of two that fits a stage
+    constexpr int EC = sizeof(typename C::Stage) >= C::NT * 64 * sizeof(float) ? 64 : 32;
+    static_assert(sizeof(typename C::Stage) >= C::NT * EC * sizeof(float), "scratch fits");
+    constexpr int NP = E / EC;  // passes per row
+    __shared__ typename C::Smem sm;
+    __shared__ uint64_t lists[LDSL ? NI * KC * C::NT : 1];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wx = wave / C::WY, wy = wave % C::WY;
     // logical id = chunk * strips + strip: an XCD's workgroups take all batch
     // strips of the same chunks, so each weight tile is read into its L2 once
-    const int64_t nb = (N + PJ_TY - 1) / PJ_TY;
+    const int64_t nb = (N + C::TY - 1) / C::TY, nt = (V + C::TX - 1) / C::TX;
     const int64_t lid = xcd_logical(blockIdx.x, per);
     if (lid >= S * nb) return;  // the whole workgroup leaves
     const int64_t c = lid / nb;
-    const int64_t y0 = (lid % nb) * PJ_TY;  // batch strip
-    const int64_t v_begin = c * tiles * PJ_TX;
-    int64_t v_end = v_begin + tiles * PJ_TX;
-    if (v_end > V) v_end = V;
+    const int64_t y0s = (lid % nb) * C::TY;  // batch strip
+    const int64_t t0 = c * tiles;
+    const int64_t t1 = t0 + tiles < nt ? t0 + tiles : nt;
 
-    float sr = kEmptyS, dacc = 0.0f;
-    uint64_t L[KC];
-    uint64_t tkey = 0ull;  // K-th key of the list (0 while it has fewer)
-    float tval = -__builtin_inff();
+    float sr[NI], dacc[NI], tval[NI];
+    uint64_t tkey[NI];  // K-th key of the list (0 while it has fewer)
+    LaneList<KC, LDSL> list[NI];
+    uint64_t* lmem[NI];
 #pragma unroll
-    for (int i = 0; i < KC; ++i) L[i] = 0ull;
+    for (int ni = 0; ni < NI; ++ni) {
+        sr[ni] = kEmptyS;
+        dacc[ni] = 0.0f;
+        tval[ni] = -__builtin_inff();
+        tkey[ni] = 0ull;
+        lmem[ni] = lists + (LDSL ? ni * KC * C::NT + threadIdx.x : 0);
+        list[ni].init(lmem[ni]);
+    }
+    float* scr = reinterpret_cast<float*>(&sm.st[1]) + threadIdx.x;  // this thread's column
 
-    for (int64_t x0 = v_begin; x0 < v_end; x0 += PJ_TX) {
-        f32x16 acc[4][1];
-        pj_tile<1, 4>(w, V, h, N, H, x0, y0, sm, acc);
-        // vocabulary entry of result register i of block mi: vbase + voff(mi, i)
-        const int64_t vbase = x0 + 4 * (lane >> 5);
-        if (x0 + PJ_TX > v_end) {  // the chunk's last tile runs past its end
-            const int64_t lim = v_end - vbase;
-#pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    if (mi * 32 + 8 * (i >> 2) + (i & 3) >= lim) acc[mi][0][i] = -__builtin_inff();
-        }
-        float lm = -__builtin_inff();
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-            for (int i = 0; i < 16; i += 2) lm = max3_raw(lm, acc[mi][0][i], acc[mi][0][i + 1]);
-        const float t = lm * kLog2e;
-        if (__builtin_amdgcn_ballot_w64(t > sr + kLazy) != 0) {
-            if (t > sr + kLazy) {
-                dacc *= exp2_hw(sr - t);
-                sr = t;
-            }
-        }
-        float dsum[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-            for (int i = 0; i < 16; ++i)
-                dsum[mi] += exp2_hw(__builtin_fmaf(acc[mi][0][i], kLog2e, -sr));
-        dacc += (dsum[0] + dsum[1]) + (dsum[2] + dsum[3]);
-        if (__builtin_amdgcn_ballot_w64(lm >= tval) != 0) {
-            // Rare path: the lane's 64 entries go to its own column of the
-            // staging LDS (free between tiles: the next tile writes it only
-            // after a workgroup barrier), and one loop walks them, so the list
-            // insertion exists once rather than per register.
-            float* scr = reinterpret_cast<float*>(&sm) + threadIdx.x;
-#pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) scr[(mi * 16 + i) * PJ_BLOCK] = acc[mi][0][i];
-            if (lm >= tval) {
-#pragma unroll 1
-                for (int j = 0; j < 64; ++j) {
-                    const float x = scr[j * PJ_BLOCK];
-                    // masked entries are -inf; a -inf logit is never a candidate
-                    if (x >= tval && x > -__builtin_inff()) {
-                        const uint32_t v = (uint32_t)(vbase + (j >> 4) * 32 +
-                                                      8 * ((j & 15) >> 2) + (j & 3));
-                        const uint64_t key = make_key(x, v);
-                        if (key > tkey) {
-                            list_insert<KC>(L, K, key);
-                            tkey = list_kth<KC>(L, K);
-                            tval = tkey != 0 ? key_value(tkey) : -__builtin_inff();
-                        }
+    pj_run<C>(
+        w, V, h, N, H, t0, t1, sm,
+        [&](int64_t t, int64_t& x0, int64_t& y0) {
+            x0 = t * C::TX;
+            y0 = y0s;
+        },
+        [&](int64_t, int64_t x0, int64_t, f32x16 (&acc)[C::MI][C::NI]) {
+            const int64_t vbase = x0 + wx * 32 * C::MI + 4 * (lane >> 5);
+            // offset from vbase of entry j (block j / 16, register j % 16)
+            auto voff = [](int j) { return (j >> 4) * 32 + 8 * ((j & 15) >> 2) + (j & 3); };
+            // Alg. 4's insertion, for an entry already known to be >= tval[ni]
+            auto offer = [&](int ni, float xv, int j) {
+                const uint64_t key = make_key(xv, (uint32_t)(vbase + voff(j)));
+                if (key > tkey[ni]) {
+                    tkey[ni] = list[ni].insert(lmem[ni], K, key);
+                    // until the list holds K keys the threshold stays as it is
+                    if (tkey[ni] != 0) tval[ni] = key_value(tkey[ni]);
+                }
+            };
+            // Alg. 3's update of the pair's reference with this tile's maximum
+            auto rescale = [&](int ni, float lm) {
+                const float tm = lm * kLog2e;
+                if (__builtin_amdgcn_ballot_w64(tm > sr[ni] + kLazy) != 0) {
+                    if (tm > sr[ni] + kLazy) {
+                        dacc[ni] *= exp2_hw(sr[ni] - tm);
+                        sr[ni] = tm;
                     }
                 }
-            }
-        }
-    }
-    const int64_t Sp = S * 2;
-    const int64_t p = c * 2 + (lane >> 5);
-    const int64_t row = y0 + wave * 32 + (lane & 31);
-    if (row < N) {
-        uint64_t* dst = pkeys + (row * Sp + p) * K;
+            };
+            // entries [q EC, q EC + EC) of row ni into this thread's LDS column
+            auto stage = [&](int ni, int q) {
 #pragma unroll
-        for (int i = 0; i < KC; ++i)
-            if (i < K) dst[i] = L[i];
-        pmd[row * Sp + p] = MD{sr, dacc};
+                for (int j = 0; j < EC; ++j)
+                    scr[j * C::NT] = acc_reread(acc[(q * EC + j) >> 4][ni][j & 15]);
+            };
+            if (x0 + C::TX > V) {
+                // The last tile of the vocabulary runs past its end (once per
+                // chunk at most): walk the row through the LDS column with a
+                // bound check, in loops, so that no mask lives in registers.
+                const int lim = (int)(V - vbase);
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) {
+                    float lm = -__builtin_inff();
+#pragma unroll
+                    for (int q = 0; q < NP; ++q) {
+                        stage(ni, q);
+#pragma unroll 1
+                        for (int j = 0; j < EC; ++j)
+                            if (voff(q * EC + j) < lim) lm = __builtin_fmaxf(lm, scr[j * C::NT]);
+                    }
+                    rescale(ni, lm);
+                    float dsum = 0.0f;
+#pragma unroll
+                    for (int q = 0; q < NP; ++q) {
+                        stage(ni, q);
+#pragma unroll 1
+                        for (int j = 0; j < EC; ++j) {
+                            if (voff(q * EC + j) >= lim) continue;
+                            const float xv = scr[j * C::NT];
+                            dsum += exp2_hw(__builtin_fmaf(xv, kLog2e, -sr[ni]));
+                            // a -inf logit is never a candidate
+                            if (xv >= tval[ni] && xv > -__builtin_inff()) offer(ni, xv, q * EC + j);
+                        }
+                    }
+                    dacc[ni] += dsum;
+                }
+                return;
+            }
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) {
+                // One pass over the row's entries: the maximum, the terms
+                // against the current reference, and for each part of EC
+                // entries a mask of the entries at or above the list's K-th
+                // value (the candidates of Alg. 4's insertion; tval only
+                // rises, so the mask holds every entry that can still enter).
+                // Only when some lane's maximum passes its reference by more
+                // than kLazy (the chunk's first tile, then rarely) does the
+                // wave move the reference and sum the terms again.
+                constexpr int NG = E / 8;  // groups of 8 entries
+                float bm[NG];              // maxima of the groups
+                float dsum[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                uint32_t cm[E / 32];  // entries below the threshold
+#pragma unroll
+                for (int u = 0; u < E / 32; ++u) cm[u] = 0u;
+#pragma unroll
+                for (int g = 0; g < NG; ++g) bm[g] = -__builtin_inff();
+                const float th = tval[ni];
+#pragma unroll
+                for (int j = 0; j < E; j += 2) {
+                    const float a0 = acc_reread(acc[j >> 4][ni][j & 15]);
+                    const float a1 = acc_reread(acc[(j + 1) >> 4][ni][(j + 1) & 15]);
+                    bm[j >> 3] = max3_raw(bm[j >> 3], a0, a1);
+                    dsum[j & 3] += exp2_hw(__builtin_fmaf(a0, kLog2e, -sr[ni]));
+                    dsum[(j + 1) & 3] += exp2_hw(__builtin_fmaf(a1, kLog2e, -sr[ni]));
+                    cm[j >> 5] |= below_bit(a0, th, j & 31) | below_bit(a1, th, (j + 1) & 31);
+                }
+                float lm = bm[0];
+#pragma unroll
+                for (int g = 1; g < NG; ++g) lm = __builtin_fmaxf(lm, bm[g]);
+                const float tm = lm * kLog2e;
+                if (__builtin_amdgcn_ballot_w64(tm > sr[ni] + kLazy) != 0) {
+                    if (tm > sr[ni] + kLazy) {
+                        dacc[ni] *= exp2_hw(sr[ni] - tm);
+                        sr[ni] = tm;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) dsum[u] = 0.0f;
+#pragma unroll
+                    for (int j = 0; j < E; ++j)
+                        dsum[j & 3] += exp2_hw(
+                            __builtin_fmaf(acc_reread(acc[j >> 4][ni][j & 15]), kLog2e, -sr[ni]));
+                }
+                dacc[ni] += (dsum[0] + dsum[1]) + (dsum[2] + dsum[3]);
+                if (__builtin_amdgcn_ballot_w64(tval[ni] == -__builtin_inff()) != 0) {
+                    // A chunk's first tile: the list is empty and every entry
+                    // would be a candidate.  The group maxima are entries of
+                    // distinct groups, so their K-th largest value (ties
+                    // counted once, which only lowers it) is a value that at
+                    // least K of the lane's entries reach: a valid threshold,
+                    // shared with the other lane holding the row.
+                    if (K <= NG && tval[ni] == -__builtin_inff()) {
+                        float b[NG], boot = -__builtin_inff();
+#pragma unroll
+                        for (int g = 0; g < NG; ++g) b[g] = bm[g];
+#pragma unroll
+                        for (int r = 0; r < NG; ++r) {
+                            if (r < K) {
+                                float m = b[0];
+#pragma unroll
+                                for (int g = 1; g < NG; ++g) m = __builtin_fmaxf(m, b[g]);
+#pragma unroll
+                                for (int g = 0; g < NG; ++g) b[g] = b[g] == m ? -__builtin_inff() : b[g];
+                                boot = m;
+                            }
+                        }
+                        tval[ni] = boot;
+                    }
+                    tval[ni] = __builtin_fmaxf(tval[ni], __shfl_xor(tval[ni], 32));
+                    const float tb = tval[ni];
+#pragma unroll
+                    for (int u = 0; u < E / 32; ++u) cm[u] = 0u;
+#pragma unroll
+                    for (int j = 0; j < E; ++j)
+                        cm[j >> 5] |= below_bit(acc_reread(acc[j >> 4][ni][j & 15]), tb, j & 31);
+                }
+#pragma unroll
+                for (int q = 0; q < NP; ++q) {
+                    uint64_t m = 0;  // candidates of this part
+#pragma unroll
+                    for (int u = 0; u < EC / 32; ++u) m |= (uint64_t)~cm[q * (EC / 32) + u] << (32 * u);
+                    if (__builtin_amdgcn_ballot_w64(m != 0) == 0) continue;
+                    // Candidates: the part goes to this thread's column of the
+                    // free LDS stage, and each lane visits only its set bits.
+                    stage(ni, q);
+                    while (m != 0) {
+                        const int j = __builtin_ctzll(m);
+                        m &= m - 1;
+                        const float xv = scr[j * C::NT];
+                        if (xv >= tval[ni]) offer(ni, xv, q * EC + j);
+                    }
+                }
+                // The other lane holding this row saw other entries of it:
+                // the larger of the two K-th values also bounds the row's
+                // K-th value from below.
+                tval[ni] = __builtin_fmaxf(tval[ni], __shfl_xor(tval[ni], 32));
+            }
+        });
+
+    constexpr int P = 2 * C::WX;  // partials per (row, chunk)
+    const int64_t Sp = S * P;
+    const int64_t p = c * P + wx * 2 + (lane >> 5);
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni) {
+        const int64_t row = y0s + wy * 32 * NI + ni * 32 + (lane & 31);
+        if (row < N) {
+            uint64_t* dst = pkeys + (row * Sp + p) * K;
+#pragma unroll
+            for (int i = 0; i < KC; ++i)
+                if (i < K) dst[i] = list[ni].get(lmem[ni], i);
+            pmd[row * Sp + p] = MD{sr[ni], dacc[ni]};
+        }
     }
 }
 
 // ---------------------------------------------------------------- launchers
-hipError_t launch_proj_logits(const void* h, const void* w, float* out, int64_t N, int64_t H,
-                              int64_t V, hipStream_t st) {
-    const int64_t total = ((N + PJ_TX - 1) / PJ_TX) * ((V + PJ_TY - 1) / PJ_TY);
+template <class C>
+static hipError_t launch_logits_t(const void* h, const void* w, float* out, int64_t N, int64_t H,
+                                  int64_t V, hipStream_t st) {
+    const int64_t total = ((N + C::TX - 1) / C::TX) * ((V + C::TY - 1) / C::TY);
     const int64_t per = (total + 7) / 8;
-    hipLaunchKernelGGL(proj_logits, dim3((unsigned)(8 * per)), dim3(PJ_BLOCK), 0, st,
+    hipLaunchKernelGGL((proj_logits<C>), dim3((unsigned)(8 * per)), dim3(C::NT), 0, st,
                        (const uint16_t*)h, (const uint16_t*)w, out, N, H, V, per);
     return hipGetLastError();
 }
 
-size_t proj_topk_part_bytes(int64_t N, int64_t S, int K) {
-    return (size_t)N * (size_t)(S * 2) * ((size_t)K * 8 + 8);
+hipError_t launch_proj_logits(const void* h, const void* w, float* out, int64_t N, int64_t H,
+                              int64_t V, int cus, hipStream_t st) {
+    const int64_t big = ((N + PjBig::TX - 1) / PjBig::TX) * ((V + PjBig::TY - 1) / PjBig::TY);
+    if (big >= 2 * (int64_t)cus) return launch_logits_t<PjBig>(h, w, out, N, H, V, st);
+    return launch_logits_t<PjSmall>(h, w, out, N, H, V, st);
+}
+
+void proj_topk_shape(int64_t N, int64_t V, int K, int cus, int64_t* S, int64_t* tiles,
+                     int* parts) {
+    const int cfg = fused_cfg(N, K);
+    const int64_t TY = cfg == 0 ? PjFused8::TY : cfg == 1 ? PjFused16::TY : PjFusedN::TY;
+    const int64_t TX = PjFused8::TX;
+    *parts = 2 * (cfg == 0 ? PjFused8::WX : cfg == 1 ? PjFused16::WX : PjFusedN::WX);
+    // vocabulary chunks: about one workgroup per CU in all (each takes 80 KB
+    // of LDS or more)
+    const int64_t nb = (N + TY - 1) / TY, nt = (V + TX - 1) / TX;
+    int64_t s = ((int64_t)cus + nb - 1) / nb;
+    if (s > nt) s = nt;
+    if (s < 1) s = 1;
+    const int64_t t = (nt + s - 1) / s;
+    *tiles = t;
+    *S = (nt + t - 1) / t;
+}
+
+size_t proj_topk_part_bytes(int64_t N, int64_t S, int parts, int K) {
+    return (size_t)N * (size_t)(S * parts) * ((size_t)K * 8 + 8);
+}
+
+template <class C, int KC, bool LDSL>
+static void launch_part(const void* h, const void* w, uint64_t* pkeys, MD* pmd, int64_t N,
+                        int64_t H, int64_t V, int K, int64_t S, int64_t tiles, hipStream_t st) {
+    const int64_t per = (S * ((N + C::TY - 1) / C::TY) + 7) / 8;
+    hipLaunchKernelGGL((proj_topk_part<C, KC, LDSL>), dim3((unsigned)(8 * per)), dim3(C::NT), 0,
+                       st, (const uint16_t*)h, (const uint16_t*)w, pkeys, pmd, N, H, V, K, S,
+                       tiles, per);
 }
 
 hipError_t launch_proj_topk(const void* h, const void* w, float* vals, int32_t* idx,
                             void* part, int64_t N, int64_t H, int64_t V, int K, int64_t S,
-                            int64_t tiles, hipStream_t st) {
+                            int64_t tiles, int parts, hipStream_t st) {
+    const int64_t Sp = S * parts;  // partials per row
     uint64_t* pkeys = static_cast<uint64_t*>(part);
-    MD* pmd = reinterpret_cast<MD*>(pkeys + N * S * 2 * K);
-    const int64_t per = (S * ((N + PJ_TY - 1) / PJ_TY) + 7) / 8;
-    dim3 grid((unsigned)(8 * per));
-    if (K <= 8)
-        hipLaunchKernelGGL((proj_topk_part<8>), grid, dim3(PJ_BLOCK), 0, st, (const uint16_t*)h,
-                           (const uint16_t*)w, pkeys, pmd, N, H, V, K, S, tiles, per);
+    MD* pmd = reinterpret_cast<MD*>(pkeys + N * Sp * K);
+    const int cfg = fused_cfg(N, K);
+    if (cfg == 0)
+        launch_part<PjFused8, 8, true>(h, w, pkeys, pmd, N, H, V, K, S, tiles, st);
+    else if (cfg == 1)
+        launch_part<PjFused16, 16, false>(h, w, pkeys, pmd, N, H, V, K, S, tiles, st);
     else
-        hipLaunchKernelGGL((proj_topk_part<16>), grid, dim3(PJ_BLOCK), 0, st, (const uint16_t*)h,
-                           (const uint16_t*)w, pkeys, pmd, N, H, V, K, S, tiles, per);
+        launch_part<PjFusedN, 16, false>(h, w, pkeys, pmd, N, H, V, K, S, tiles, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     constexpr int WB = TK_BLOCK / 64;
     dim3 mgrid((unsigned)((N + WB - 1) / WB));
     hipLaunchKernelGGL((topk_merge<TK_ONLINE>), mgrid, dim3(TK_BLOCK), 0, st, pkeys, pmd, vals,
-                       idx, N, S * 2, K);
+                       idx, N, Sp, K);
     return hipGetLastError();
 }
 

@@ -134,3 +134,31 @@ def test_proj_topk_deterministic(dev):
     b = osm.proj_softmax_topk(h, w, 8)
     torch.cuda.synchronize()
     assert torch.equal(a[1], b[1]) and torch.equal(a[0].view(torch.int32), b[0].view(torch.int32))
+
+
+@pytest.mark.parametrize("K", [1, 2, 5, 16])
+def test_proj_topk_all_equal_logits(dev, K):
+    """w = 0: every logit is exactly 0, so the top-k is the K lowest indices
+    (ties in increasing index order) and each value is exactly 1 / V."""
+    N, H, V = 70, 64, 3000
+    h, _ = random_inputs(N, H, V, seed=K, dev=dev)
+    w = torch.zeros(V, H, dtype=torch.bfloat16, device=dev)
+    vals, idx = osm.proj_softmax_topk(h, w, K)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(idx), np.tile(np.arange(K, dtype=np.int32), (N, 1)))
+    assert_softmax_close(to_host(vals), np.full((N, K), 1.0 / V), "all-equal logits")
+
+
+@pytest.mark.parametrize("N", [64, 65, 128, 129, 257])
+@pytest.mark.parametrize("K", [5, 9, 16])
+def test_proj_topk_tile_shapes(dev, N, K):
+    """Batch sizes on each side of the fused kernel's tile choices (256 x 64,
+    256 x 128 and 256 x 256 tiles), with a ragged last vocabulary tile and a
+    K that is not a multiple of the 64-element step."""
+    H, V = 136, 3001
+    h, w = exact_inputs(N, H, V, seed=N * 31 + K, dev=dev)
+    vals, idx = osm.proj_softmax_topk(h, w, K)
+    torch.cuda.synchronize()
+    v64, z64 = oracle.topk(oracle_logits(h, w), K, "f64")
+    assert np.array_equal(to_host(idx), z64)
+    assert_softmax_close(to_host(vals), v64, f"tile shapes N={N} K={K}")
