@@ -82,6 +82,8 @@ __global__ __launch_bounds__(C::NT) void proj_logits(const uint16_t* __restrict_
 }
 
 // ------------------------------------------------------------ fused top-k
+constexpr int64_t PJ_CB = 4, PJ_SB = 8;  // block of chunks x batch strips per XCD
+
 // Insert `key` into a lane's list (descending, K valid entries in a
 // register array of KC, unused entries 0); the caller has checked that key
 // exceeds the K-th entry.  Every entry moves at most one place, computed
@@ -183,18 +185,22 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
     // entries per pass of the LDS column: the largest power of two that fits a stage
     constexpr int EC = sizeof(typename C::Stage) >= C::NT * 64 * sizeof(float) ? 64 : 32;
     static_assert(sizeof(typename C::Stage) >= C::NT * EC * sizeof(float), "scratch fits");
-    constexpr int NP = E / EC;  // passes per row
     __shared__ typename C::Smem sm;
     __shared__ uint64_t lists[LDSL ? NI * KC * C::NT : 1];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wx = wave / C::WY, wy = wave % C::WY;
-    // logical id = chunk * strips + strip: an XCD's workgroups take all batch
-    // strips of the same chunks, so each weight tile is read into its L2 once
+    // Logical ids in blocks of PJ_CB chunks x up to PJ_SB batch strips, so
+    // that the workgroups of an XCD (a contiguous range of ids) share few
+    // operand tiles in its L2: a block of 4 x 8 reads 12 distinct tiles per
+    // step where 2 chunks x 16 strips would read 18.
     const int64_t nb = (N + C::TY - 1) / C::TY, nt = (V + C::TX - 1) / C::TX;
+    const int64_t sb = nb < PJ_SB ? nb : PJ_SB, nsb = (nb + sb - 1) / sb;
     const int64_t lid = xcd_logical(blockIdx.x, per);
-    if (lid >= S * nb) return;  // the whole workgroup leaves
-    const int64_t c = lid / nb;
-    const int64_t y0s = (lid % nb) * C::TY;  // batch strip
+    const int64_t blk = lid / (PJ_CB * sb), in = lid % (PJ_CB * sb);
+    const int64_t c = (blk / nsb) * PJ_CB + in / sb;
+    const int64_t strip = (blk % nsb) * sb + in % sb;
+    if (c >= S || strip >= nb) return;  // the whole workgroup leaves
+    const int64_t y0s = strip * C::TY;  // batch strip
     const int64_t t0 = c * tiles;
     const int64_t t1 = t0 + tiles < nt ? t0 + tiles : nt;
 
@@ -220,6 +226,8 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
             y0 = y0s;
         },
         [&](int64_t, int64_t x0, int64_t, f32x16 (&acc)[C::MI][C::NI]) {
+            constexpr int E = C::MI * 16;  // entries per row per lane
+            constexpr int NG = E / 8;      // groups of 8 entries
             const int64_t vbase = x0 + wx * 32 * C::MI + 4 * (lane >> 5);
             // offset from vbase of entry j (block j / 16, register j % 16)
             auto voff = [](int j) { return (j >> 4) * 32 + 8 * ((j & 15) >> 2) + (j & 3); };
@@ -232,148 +240,129 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
                     if (tkey[ni] != 0) tval[ni] = key_value(tkey[ni]);
                 }
             };
-            // Alg. 3's update of the pair's reference with this tile's maximum
-            auto rescale = [&](int ni, float lm) {
-                const float tm = lm * kLog2e;
-                if (__builtin_amdgcn_ballot_w64(tm > sr[ni] + kLazy) != 0) {
-                    if (tm > sr[ni] + kLazy) {
-                        dacc[ni] *= exp2_hw(sr[ni] - tm);
-                        sr[ni] = tm;
-                    }
-                }
-            };
             // entries [q EC, q EC + EC) of row ni into this thread's LDS column
             auto stage = [&](int ni, int q) {
 #pragma unroll
                 for (int j = 0; j < EC; ++j)
                     scr[j * C::NT] = acc_reread(acc[(q * EC + j) >> 4][ni][j & 15]);
             };
-            if (x0 + C::TX > V) {
-                // The last tile of the vocabulary runs past its end (once per
-                // chunk at most): walk the row through the LDS column with a
-                // bound check, in loops, so that no mask lives in registers.
-                const int lim = (int)(V - vbase);
-#pragma unroll
-                for (int ni = 0; ni < NI; ++ni) {
-                    float lm = -__builtin_inff();
-#pragma unroll
-                    for (int q = 0; q < NP; ++q) {
-                        stage(ni, q);
-#pragma unroll 1
-                        for (int j = 0; j < EC; ++j)
-                            if (voff(q * EC + j) < lim) lm = __builtin_fmaxf(lm, scr[j * C::NT]);
-                    }
-                    rescale(ni, lm);
-                    float dsum = 0.0f;
-#pragma unroll
-                    for (int q = 0; q < NP; ++q) {
-                        stage(ni, q);
-#pragma unroll 1
-                        for (int j = 0; j < EC; ++j) {
-                            if (voff(q * EC + j) >= lim) continue;
-                            const float xv = scr[j * C::NT];
-                            dsum += exp2_hw(__builtin_fmaf(xv, kLog2e, -sr[ni]));
-                            // a -inf logit is never a candidate
-                            if (xv >= tval[ni] && xv > -__builtin_inff()) offer(ni, xv, q * EC + j);
-                        }
-                    }
-                    dacc[ni] += dsum;
-                }
-                return;
-            }
+            // The vocabulary's last tile may run past V (once per chunk at
+            // most): entries at offsets >= lim do not exist.
+            const bool ragged = x0 + C::TX > V;
+            const int lim = ragged ? (int)(V - vbase) : 1 << 30;
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni) {
-                // One pass over the row's entries: the maximum, the terms
-                // against the current reference, and for each part of EC
-                // entries a mask of the entries at or above the list's K-th
-                // value (the candidates of Alg. 4's insertion; tval only
-                // rises, so the mask holds every entry that can still enter).
-                // Only when some lane's maximum passes its reference by more
-                // than kLazy (the chunk's first tile, then rarely) does the
-                // wave move the reference and sum the terms again.
-                constexpr int NG = E / 8;  // groups of 8 entries
-                float bm[NG];              // maxima of the groups
+                // 1. One pass over the row's entries (the only code unrolled
+                //    over them): the maxima of groups of 8, the terms against
+                //    the current reference and the entries below the list's
+                //    K-th value (tval only rises, so every entry that can still
+                //    enter the list is outside that set).
+                float bm[NG];
                 float dsum[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                uint32_t cm[E / 32];  // entries below the threshold
-#pragma unroll
-                for (int u = 0; u < E / 32; ++u) cm[u] = 0u;
+                uint32_t cm[E / 32];
 #pragma unroll
                 for (int g = 0; g < NG; ++g) bm[g] = -__builtin_inff();
-                const float th = tval[ni];
 #pragma unroll
-                for (int j = 0; j < E; j += 2) {
-                    const float a0 = acc_reread(acc[j >> 4][ni][j & 15]);
-                    const float a1 = acc_reread(acc[(j + 1) >> 4][ni][(j + 1) & 15]);
-                    bm[j >> 3] = max3_raw(bm[j >> 3], a0, a1);
-                    dsum[j & 3] += exp2_hw(__builtin_fmaf(a0, kLog2e, -sr[ni]));
-                    dsum[(j + 1) & 3] += exp2_hw(__builtin_fmaf(a1, kLog2e, -sr[ni]));
-                    cm[j >> 5] |= below_bit(a0, th, j & 31) | below_bit(a1, th, (j + 1) & 31);
+                for (int u = 0; u < E / 32; ++u) cm[u] = 0u;
+                if (!ragged) {
+                    const float th = tval[ni];
+#pragma unroll
+                    for (int j = 0; j < E; j += 2) {
+                        const float a0 = acc_reread(acc[j >> 4][ni][j & 15]);
+                        const float a1 = acc_reread(acc[(j + 1) >> 4][ni][(j + 1) & 15]);
+                        bm[j >> 3] = max3_raw(bm[j >> 3], a0, a1);
+                        dsum[j & 3] += exp2_hw(__builtin_fmaf(a0, kLog2e, -sr[ni]));
+                        dsum[(j + 1) & 3] += exp2_hw(__builtin_fmaf(a1, kLog2e, -sr[ni]));
+                        cm[j >> 5] |= below_bit(a0, th, j & 31) | below_bit(a1, th, (j + 1) & 31);
+                    }
+                } else {
+#pragma unroll
+                    for (int j = 0; j < E; ++j) {
+                        const float a = acc_reread(acc[j >> 4][ni][j & 15]);
+                        bm[j >> 3] = __builtin_fmaxf(bm[j >> 3], voff(j) < lim ? a : -__builtin_inff());
+                    }
                 }
                 float lm = bm[0];
 #pragma unroll
                 for (int g = 1; g < NG; ++g) lm = __builtin_fmaxf(lm, bm[g]);
+                // 2. Alg. 3: move the reference when some lane's maximum
+                //    passes it by more than kLazy (the chunk's first tile, then
+                //    rarely); the terms are then summed again below.
+                bool recompute = ragged;
                 const float tm = lm * kLog2e;
                 if (__builtin_amdgcn_ballot_w64(tm > sr[ni] + kLazy) != 0) {
                     if (tm > sr[ni] + kLazy) {
                         dacc[ni] *= exp2_hw(sr[ni] - tm);
                         sr[ni] = tm;
                     }
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) dsum[u] = 0.0f;
-#pragma unroll
-                    for (int j = 0; j < E; ++j)
-                        dsum[j & 3] += exp2_hw(
-                            __builtin_fmaf(acc_reread(acc[j >> 4][ni][j & 15]), kLog2e, -sr[ni]));
+                    recompute = true;
                 }
-                dacc[ni] += (dsum[0] + dsum[1]) + (dsum[2] + dsum[3]);
+                // 3. A chunk's first tile: the list is empty and every entry
+                //    would be a candidate.  The group maxima are entries of
+                //    distinct groups, so their K-th largest value (ties counted
+                //    once, which only lowers it) is a value that at least K of
+                //    the lane's entries reach: a valid threshold, shared with
+                //    the other lane holding the row.  The candidates are then
+                //    found again below.
+                bool remask = ragged;
                 if (__builtin_amdgcn_ballot_w64(tval[ni] == -__builtin_inff()) != 0) {
-                    // A chunk's first tile: the list is empty and every entry
-                    // would be a candidate.  The group maxima are entries of
-                    // distinct groups, so their K-th largest value (ties
-                    // counted once, which only lowers it) is a value that at
-                    // least K of the lane's entries reach: a valid threshold,
-                    // shared with the other lane holding the row.
                     if (K <= NG && tval[ni] == -__builtin_inff()) {
                         float b[NG], boot = -__builtin_inff();
 #pragma unroll
                         for (int g = 0; g < NG; ++g) b[g] = bm[g];
+#pragma unroll 1
+                        for (int r = 0; r < K; ++r) {
+                            float m = b[0];
 #pragma unroll
-                        for (int r = 0; r < NG; ++r) {
-                            if (r < K) {
-                                float m = b[0];
+                            for (int g = 1; g < NG; ++g) m = __builtin_fmaxf(m, b[g]);
 #pragma unroll
-                                for (int g = 1; g < NG; ++g) m = __builtin_fmaxf(m, b[g]);
-#pragma unroll
-                                for (int g = 0; g < NG; ++g) b[g] = b[g] == m ? -__builtin_inff() : b[g];
-                                boot = m;
-                            }
+                            for (int g = 0; g < NG; ++g) b[g] = b[g] == m ? -__builtin_inff() : b[g];
+                            boot = m;
                         }
                         tval[ni] = boot;
                     }
                     tval[ni] = __builtin_fmaxf(tval[ni], __shfl_xor(tval[ni], 32));
-                    const float tb = tval[ni];
-#pragma unroll
-                    for (int u = 0; u < E / 32; ++u) cm[u] = 0u;
-#pragma unroll
-                    for (int j = 0; j < E; ++j)
-                        cm[j >> 5] |= below_bit(acc_reread(acc[j >> 4][ni][j & 15]), tb, j & 31);
+                    remask = true;
                 }
+                float ds = recompute ? 0.0f : (dsum[0] + dsum[1]) + (dsum[2] + dsum[3]);
+                // 4. Per part of EC entries, when anything is left to do, the
+                //    part goes to this thread's column of the free LDS stage
+                //    (the one copy of the part's registers in the code), and
+                //    rolled loops finish the work: the terms again after a
+                //    move of the reference, the candidates again after the
+                //    bootstrap or on the ragged tile (with the bound), then
+                //    Alg. 4's insertion of each candidate.
 #pragma unroll
-                for (int q = 0; q < NP; ++q) {
+                for (int q = 0; q < E / EC; ++q) {
                     uint64_t m = 0;  // candidates of this part
 #pragma unroll
                     for (int u = 0; u < EC / 32; ++u) m |= (uint64_t)~cm[q * (EC / 32) + u] << (32 * u);
-                    if (__builtin_amdgcn_ballot_w64(m != 0) == 0) continue;
-                    // Candidates: the part goes to this thread's column of the
-                    // free LDS stage, and each lane visits only its set bits.
+                    if (!recompute && !remask && __builtin_amdgcn_ballot_w64(m != 0) == 0) continue;
                     stage(ni, q);
+                    if (recompute || remask) {
+                        const float tv = tval[ni], s = sr[ni];
+                        uint64_t nm = 0;
+                        float pd = 0.0f;
+#pragma unroll 4
+                        for (int j = 0; j < EC; ++j) {
+                            const float xv = scr[j * C::NT];
+                            const bool valid = voff(q * EC + j) < lim;
+                            const float e = exp2_hw(__builtin_fmaf(xv, kLog2e, -s));
+                            pd += valid ? e : 0.0f;
+                            nm |= (uint64_t)(valid && xv >= tv) << j;
+                        }
+                        if (recompute) ds += pd;
+                        if (remask) m = nm;
+                    }
                     while (m != 0) {
                         const int j = __builtin_ctzll(m);
                         m &= m - 1;
                         const float xv = scr[j * C::NT];
-                        if (xv >= tval[ni]) offer(ni, xv, q * EC + j);
+                        // a -inf logit is never a candidate
+                        if (xv >= tval[ni] && xv > -__builtin_inff()) offer(ni, xv, q * EC + j);
                     }
                 }
+                dacc[ni] += ds;
                 // The other lane holding this row saw other entries of it:
                 // the larger of the two K-th values also bounds the row's
                 // K-th value from below.
@@ -439,7 +428,10 @@ size_t proj_topk_part_bytes(int64_t N, int64_t S, int parts, int K) {
 template <class C, int KC, bool LDSL>
 static void launch_part(const void* h, const void* w, uint64_t* pkeys, MD* pmd, int64_t N,
                         int64_t H, int64_t V, int K, int64_t S, int64_t tiles, hipStream_t st) {
-    const int64_t per = (S * ((N + C::TY - 1) / C::TY) + 7) / 8;
+    const int64_t nb = (N + C::TY - 1) / C::TY;
+    const int64_t sb = nb < PJ_SB ? nb : PJ_SB, nsb = (nb + sb - 1) / sb;
+    const int64_t ids = (S + PJ_CB - 1) / PJ_CB * nsb * PJ_CB * sb;  // whole blocks
+    const int64_t per = (ids + 7) / 8;
     hipLaunchKernelGGL((proj_topk_part<C, KC, LDSL>), dim3((unsigned)(8 * per)), dim3(C::NT), 0,
                        st, (const uint16_t*)h, (const uint16_t*)w, pkeys, pmd, N, H, V, K, S,
                        tiles, per);
