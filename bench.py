@@ -160,6 +160,23 @@ def copy_probe():
         f"{2 * n * 4 / (median(t) * 1e-3) / 1e9:.0f} GB/s (read+write)")
 
 
+def proj_probe(osm):
+    """The projection and the fused projection + softmax + top-5 at
+    4000 x 4096 x 128256 (bfloat16 h, w), three calls each, for kernel
+    statistics and counters under a profiler."""
+    import torch
+    N, H, V = 4000, 4096, 128256
+    g = torch.Generator(device="cuda").manual_seed(0)
+    h = torch.randn(N, H, device="cuda", generator=g).to(torch.bfloat16)
+    w = (torch.randn(V, H, device="cuda", generator=g) / H ** 0.5).to(torch.bfloat16)
+    out = torch.empty(N, V, device="cuda")
+    for _ in range(3):
+        osm.proj(h, w, out)
+        osm.proj_softmax_topk(h, w, 5)
+    torch.cuda.synchronize()
+    log("proj probe done")
+
+
 def sweep(path: str):
     """Every workload shape, the paper's V sweeps at batch 4000 and 10, and
     its K sweep: one JSON record per (shape, op) into `path`.  Each record is
@@ -265,6 +282,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--proj-probe", action="store_true")
     ap.add_argument("--compare-reps", type=int, default=20)
     ap.add_argument("--sweep", metavar="FILE", help="time every workload shape and the V "
                     "sweeps; one JSON record per line into FILE")
@@ -284,6 +302,9 @@ def main():
     osm.lib()  # fail loudly if the HIP library is not built
     if args.copy_probe:
         copy_probe()
+        return
+    if args.proj_probe:
+        proj_probe(osm)
         return
     if args.sweep:
         sweep(args.sweep)
