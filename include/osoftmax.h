@@ -93,9 +93,15 @@ enum osm_kernel {
                              four wavefronts per row). */
     OSM_KERNEL_SPLIT = 2  /* param = chunks per row S >= 1: a workgroup per
                              chunk; per-chunk normalizer pairs (and, for
-                             top-k, per-chunk top-k keys) are merged in a
-                             second kernel through a scratch array
-                             (stream-ordered allocation) */
+                             top-k, per-chunk top-k keys) go through a
+                             scratch array (stream-ordered allocation).
+                             Softmax merges them in a second kernel; top-k
+                             merges each row in the workgroup that completes
+                             it, counted in a per-stream array of N
+                             counters that is cleared once when allocated
+                             and left cleared by every call (so calls on one
+                             stream must not overlap, which stream order
+                             guarantees) */
 };
 
 /* Softmax + top-k algorithms (Section 4, and the comparisons of Section 5.2):
@@ -166,7 +172,7 @@ OSM_API int softmax_topk_dt(const void* x, float* vals, int32_t* idx, int64_t N,
  * within binary32 rounding of the reduction tree.
  * Errors: as softmax_topk_dt, plus OSM_EINVAL for another kernel or param,
  * or N * S >= 2^31 chunks; OSM_ENOMEM if the split scratch (N * S * (8K + 8)
- * bytes) cannot be allocated. */
+ * bytes) or the row counters (4N bytes) cannot be allocated. */
 OSM_API int softmax_topk_ex(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V,
                             int K, int dtype, int kernel, int64_t param, hipStream_t stream);
 

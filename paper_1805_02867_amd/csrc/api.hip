@@ -33,9 +33,11 @@ struct DeviceState {
     int cus = 0;
     hipMemPool_t pool = nullptr;
     bool pool_ok = false;
-    std::mutex mu;  // guards the scratch table
+    std::mutex mu;  // guards the scratch and counter tables
     ScratchSlot slots[kScratchSlots] = {};
     int nslots = 0;
+    ScratchSlot cslots[kScratchSlots] = {};  // zeroed counter arrays, per stream
+    int ncslots = 0;
 };
 DeviceState g_dev[kMaxDevices];
 
@@ -104,6 +106,49 @@ int acquire_scratch(DeviceState* ds, hipStream_t stream, size_t bytes, void** ou
         slot->bytes = want;
     }
     *out = p;
+    return OSM_OK;
+}
+
+// A zeroed array of at least `count` 32-bit counters for work enqueued on
+// `stream`; the kernels that use it leave it zeroed.  A stream's array grows
+// by a stream-ordered allocation, cleared in stream order; once the table is
+// full, a call gets an array of its own (*temp = true) to free after its
+// launches.
+int acquire_counters(DeviceState* ds, hipStream_t stream, size_t count, uint32_t** out,
+                     bool* temp) {
+    if (!ds->pool_ok) return OSM_ENOMEM;
+    std::lock_guard<std::mutex> guard(ds->mu);
+    ScratchSlot* slot = nullptr;
+    for (int i = 0; i < ds->ncslots; ++i)
+        if (ds->cslots[i].stream == stream) slot = &ds->cslots[i];
+    if (!slot && ds->ncslots < kScratchSlots) {
+        slot = &ds->cslots[ds->ncslots++];
+        *slot = ScratchSlot{stream, nullptr, 0};
+    }
+    *temp = slot == nullptr;
+    const size_t bytes = count * 4;
+    if (slot && slot->bytes >= bytes) {
+        *out = static_cast<uint32_t*>(slot->ptr);
+        return OSM_OK;
+    }
+    size_t want = bytes;
+    if (slot) want = bytes > 2 * slot->bytes ? bytes : 2 * slot->bytes;
+    void* p = nullptr;
+    if (hipMallocFromPoolAsync(&p, want, ds->pool, stream) != hipSuccess || !p) {
+        (void)hipGetLastError();
+        return OSM_ENOMEM;
+    }
+    if (hipMemsetAsync(p, 0, want, stream) != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFreeAsync(p, stream);
+        return OSM_EHIP;
+    }
+    if (slot) {
+        if (slot->ptr) (void)hipFreeAsync(slot->ptr, stream);
+        slot->ptr = p;
+        slot->bytes = want;
+    }
+    *out = static_cast<uint32_t*>(p);
     return OSM_OK;
 }
 
@@ -277,15 +322,24 @@ int launch_topk_pass(const void* x, float* vals, int32_t* idx, int64_t N, int64_
     }
     void* scratch = nullptr;
     bool temp = false;
-    const int st = acquire_scratch(ds, stream, osm::topk_part_bytes(N, S, K), &scratch, &temp);
+    int st = acquire_scratch(ds, stream, osm::topk_part_bytes(N, S, K), &scratch, &temp);
     if (st != OSM_OK) return st;
     a.part = scratch;
     a.S = S;
     a.chunk = chunk;
+    // per-row chunk counters: each row's last chunk merges it in the same kernel
+    bool ctemp = false;
+    st = acquire_counters(ds, stream, (size_t)N, &a.ctr, &ctemp);
+    if (st != OSM_OK) {
+        if (temp) (void)hipFreeAsync(scratch, stream);
+        return st;
+    }
     hipError_t e = osm::launch_topk(a, dtype, var);
     hipError_t f = temp ? hipFreeAsync(scratch, stream) : hipSuccess;
+    hipError_t g = ctemp ? hipFreeAsync(a.ctr, stream) : hipSuccess;
     if (e != hipSuccess) return OSM_EHIP;
-    return hip_status(f);
+    if (f != hipSuccess) return hip_status(f);
+    return hip_status(g);
 }
 
 bool topk_algo_ok(int algo) {

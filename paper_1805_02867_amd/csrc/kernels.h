@@ -60,6 +60,10 @@ struct TopkLaunch {
     int waves_per_row;   // S <= 1: 1, 2 (TK_ONLINE only) or 4
     int64_t S, chunk;    // chunks per row and their length in elements (S > 1)
     hipStream_t st;
+    // S > 1: N zeroed per-row counters, so that each row's last chunk merges
+    // the row in the same kernel (the counters are left zeroed); null: a
+    // second kernel merges.
+    uint32_t* ctr = nullptr;
 };
 
 // Split scratch: N * S * K 64-bit keys, then N * S normalizer pairs.

@@ -409,38 +409,50 @@ __device__ __forceinline__ float sum_exp_fixed(float d, const float (&x)[N], flo
 // outputs (segs must be 1); PART = true writes, per virtual row, its K
 // largest keys (indices relative to the start of the row; 0 = fewer than K)
 // and its normalizer pair, which topk_merge combines.
-template <typename T, int W, int U, int VAR, bool PART>
-__global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
-                                                      float* __restrict__ vals,
-                                                      int32_t* __restrict__ idx,
-                                                      uint64_t* __restrict__ pkeys,
-                                                      MD* __restrict__ pmd, int64_t N, int64_t V,
-                                                      int K, int64_t seg, int64_t segs) {
+// LDS slots of one wavefront's list + queue region for a shape: the
+// candidate path checks the selection trigger after its first UH = U / 2
+// vectors and again at the end of the step, so at most max(UH, U - UH) * E
+// keys per lane are appended between two checks.
+template <typename T, int U>
+constexpr int topk_region() {
+    constexpr int E = Vec<T>::N, UH = U / 2;
+    return region_slots(64 * E * (UH > U - UH ? UH : U - UH));
+}
+
+// The LDS of a workgroup of the fused top-k kernels.
+template <typename T, int U>
+struct TopkSmem {
+    uint64_t region[TK_BLOCK / 64][topk_region<T, U>()];
+    uint64_t published[TK_BLOCK / 64];
+    MD wmd[TK_BLOCK / 64];
+    float wmx[TK_BLOCK / 64];
+};
+
+// One (virtual) row by the W wavefronts of this thread's row group: row vr,
+// or with PART chunk vr % segs (seg elements) of row vr / segs, whose K
+// largest keys and pair go to pkeys[vr * K ...] and pmd[vr].  The caller has
+// emptied the group's lists and thresholds (and, for W > 1, synchronised).
+// Returns whether this wavefront holds the row's result (all of them for
+// W = 1, the row's first for W > 1).  COH: the partial is stored with
+// agent-scope atomic stores, which reach the device's coherence point
+// without cache maintenance, for another workgroup of the same kernel.
+template <typename T, int W, int U, int VAR, bool PART, bool COH = false>
+__device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restrict__ x,
+                                          float* __restrict__ vals, int32_t* __restrict__ idx,
+                                          uint64_t* __restrict__ pkeys, MD* __restrict__ pmd,
+                                          int64_t V, int K, int64_t seg, int64_t segs,
+                                          int64_t vr) {
     constexpr int E = Vec<T>::N;
-    constexpr int WB = TK_BLOCK / 64;       // wavefronts per workgroup
-    constexpr int RB = WB / W;              // rows per workgroup
     constexpr int TR = 64 * W;              // threads per row
     constexpr int64_t STEP = (int64_t)TR * U;
-    // The candidate path checks the selection trigger after its first UH
-    // vectors and again at the end of the step, so at most
-    // max(UH, U - UH) * E keys per lane are appended between two checks.
     constexpr int UH = U / 2;
-    constexpr int REGION = region_slots(64 * E * (UH > U - UH ? UH : U - UH));
-    __shared__ uint64_t region[WB][REGION];
-    __shared__ uint64_t published[WB];
-    __shared__ MD wmd[WB];
-    __shared__ float wmx[WB];
-
+    auto& region = sm.region;
+    auto& wmd = sm.wmd;
+    auto& wmx = sm.wmx;
+    uint64_t* const published = sm.published;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int rw = wv % W;                  // wavefront within the row
     const int tr = tid % TR;                // thread within the row
-    const int64_t vr = (int64_t)blockIdx.x * RB + wv / W;
-    const bool live = vr < N * segs;        // uniform per wavefront (and per row)
-
-    if (lane < K) region[wv][lane] = 0;     // empty list
-    if (lane == 0) published[wv] = 0;
-    if constexpr (W > 1) __syncthreads();
-    if (!live) return;                      // whole rows leave together
 
     const int64_t row = PART ? vr / segs : vr;
     const int64_t start = PART ? (vr - row * segs) * seg : 0;
@@ -691,7 +703,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
     if constexpr (W > 1) {
         if (lane == 0) wmd[wv] = md;
         __syncthreads();
-        if (rw != 0) return;
+        if (rw != 0) return false;
         const int w0 = wv;  // first wavefront of the row
         md = wmd[w0];
 #pragma unroll
@@ -703,8 +715,18 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
         key = select_topk<W>(e, W, K, &found);
     }
     if constexpr (PART) {
-        if (lane < K) pkeys[vr * K + lane] = key;
-        if (VAR != TK_VALUES && lane == 0) pmd[vr] = md;
+        if constexpr (COH) {
+            if (lane < K)
+                __hip_atomic_store(pkeys + vr * K + lane, key, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            if (VAR != TK_VALUES && lane == 0)
+                __hip_atomic_store(reinterpret_cast<uint64_t*>(pmd + vr),
+                                   __builtin_bit_cast(uint64_t, md), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            if (lane < K) pkeys[vr * K + lane] = key;
+            if (VAR != TK_VALUES && lane == 0) pmd[vr] = md;
+        }
     } else if (lane < K) {
         if constexpr (VAR == TK_VALUES) {
             vals[row * K + lane] = key_value(key);
@@ -714,6 +736,26 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
         }
         idx[row * K + lane] = key_index(key);
     }
+    return true;
+}
+
+template <typename T, int W, int U, int VAR, bool PART>
+__global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
+                                                      float* __restrict__ vals,
+                                                      int32_t* __restrict__ idx,
+                                                      uint64_t* __restrict__ pkeys,
+                                                      MD* __restrict__ pmd, int64_t N, int64_t V,
+                                                      int K, int64_t seg, int64_t segs) {
+    constexpr int RB = TK_BLOCK / 64 / W;   // rows per workgroup
+    __shared__ TopkSmem<T, U> sm;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int64_t vr = (int64_t)blockIdx.x * RB + wv / W;
+    const bool live = vr < N * segs;        // uniform per wavefront (and per row)
+    if (lane < K) sm.region[wv][lane] = 0;  // empty list
+    if (lane == 0) sm.published[wv] = 0;
+    if constexpr (W > 1) __syncthreads();
+    if (!live) return;                      // whole rows leave together
+    topk_vrow<T, W, U, VAR, PART>(sm, x, vals, idx, pkeys, pmd, V, K, seg, segs, vr);
 }
 
 // Second stage of the split top-k: per row, the K largest of the S * K
@@ -721,6 +763,62 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
 // kernel) and the fixed-order merge (Eq. 4) of the S chunk pairs.  One
 // wavefront per row.
 constexpr int TK_MERGE_B = 8;  // keys per lane in flight
+
+// One row by one wavefront: region holds region_slots(64 * B) slots, its
+// first K already empty; B keys per lane are in flight.  COH: the partials
+// are read with agent-scope atomic loads (written by other workgroups of the
+// same kernel).
+template <int VAR, bool COH = false, int B = TK_MERGE_B>
+__device__ __forceinline__ void topk_merge_row(uint64_t* region, const uint64_t* pkeys,
+                                               const MD* pmd, float* __restrict__ vals,
+                                               int32_t* __restrict__ idx, int64_t row, int64_t S,
+                                               int K) {
+    const int lane = threadIdx.x & 63;
+    TopkWave<1> tw{region, nullptr, 0, K, 0, 0ull, -__builtin_inff(), 0ull};
+    const int fa = flush_at(K);
+    const int64_t n = S * K;
+    const uint64_t* pk = pkeys + row * n;
+    for (int64_t c = 0; c < n; c += 64 * B) {
+        uint64_t k[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const int64_t j = c + b * 64 + lane;
+            if constexpr (COH)
+                k[b] = j < n ? __hip_atomic_load(pk + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                             : 0ull;
+            else
+                k[b] = j < n ? pk[j] : 0ull;
+        }
+#pragma unroll
+        for (int b = 0; b < B; ++b) tw.append(k[b] > tw.tau, k[b]);  // 0 never passes
+        if (tw.qcount >= fa) tw.flush();
+    }
+    tw.flush();
+    const uint64_t key = tw.mine;
+    MD md = md_empty();
+    if constexpr (VAR != TK_VALUES) {
+        for (int64_t j = lane; j < S; j += 64) {
+            MD p;
+            if constexpr (COH)
+                p = __builtin_bit_cast(MD, __hip_atomic_load(
+                                               reinterpret_cast<const uint64_t*>(pmd + row * S + j),
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+            else
+                p = pmd[row * S + j];
+            md = md_merge(md, p);
+        }
+        md = group_merge<64>(md);  // every lane takes part
+    }
+    if (lane < K) {
+        if constexpr (VAR == TK_VALUES) {
+            vals[row * K + lane] = key_value(key);
+        } else {
+            const float Sv = md.s, rd = 1.0f / md.d;
+            vals[row * K + lane] = exp2_hw(__builtin_fmaf(key_value(key), kLog2e, -Sv)) * rd;
+        }
+        idx[row * K + lane] = key_index(key);
+    }
+}
 
 template <int VAR>
 __global__ __launch_bounds__(TK_BLOCK) void topk_merge(const uint64_t* __restrict__ pkeys,
@@ -735,37 +833,49 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_merge(const uint64_t* __restric
     const int64_t row = (int64_t)blockIdx.x * WB + wv;
     if (lane < K) region[wv][lane] = 0;
     if (row >= N) return;
-    TopkWave<1> tw{region[wv], nullptr, 0, K, 0, 0ull, -__builtin_inff(), 0ull};
-    const int fa = flush_at(K);
-    const int64_t n = S * K;
-    const uint64_t* pk = pkeys + row * n;
-    for (int64_t c = 0; c < n; c += 64 * TK_MERGE_B) {
-        uint64_t k[TK_MERGE_B];
-#pragma unroll
-        for (int b = 0; b < TK_MERGE_B; ++b) {
-            const int64_t j = c + b * 64 + lane;
-            k[b] = j < n ? pk[j] : 0ull;
-        }
-#pragma unroll
-        for (int b = 0; b < TK_MERGE_B; ++b) tw.append(k[b] > tw.tau, k[b]);  // 0 never passes
-        if (tw.qcount >= fa) tw.flush();
-    }
-    tw.flush();
-    const uint64_t key = tw.mine;
-    MD md = md_empty();
-    if constexpr (VAR != TK_VALUES) {
-        for (int64_t j = lane; j < S; j += 64) md = md_merge(md, pmd[row * S + j]);
-        md = group_merge<64>(md);  // every lane takes part
-    }
-    if (lane < K) {
-        if constexpr (VAR == TK_VALUES) {
-            vals[row * K + lane] = key_value(key);
-        } else {
-            const float Sv = md.s, rd = 1.0f / md.d;
-            vals[row * K + lane] = exp2_hw(__builtin_fmaf(key_value(key), kLog2e, -Sv)) * rd;
-        }
-        idx[row * K + lane] = key_index(key);
-    }
+    topk_merge_row<VAR>(region[wv], pkeys, pmd, vals, idx, row, S, K);
+}
+
+// Split top-k in one kernel: chunk c of row r is workgroup r * segs + c (four
+// wavefronts), which leaves its partial (K keys, pair) at the coherence
+// point; the workgroup that completes a row (ctr[r] counts its chunks) merges
+// the row's partials there and then, instead of a second kernel.  ctr starts
+// at zero and is left at zero (the merger resets its row's count).
+template <typename T, int U, int VAR>
+__global__ __launch_bounds__(TK_BLOCK) void topk_split1(const T* __restrict__ x,
+                                                       float* __restrict__ vals,
+                                                       int32_t* __restrict__ idx,
+                                                       uint64_t* __restrict__ pkeys,
+                                                       MD* __restrict__ pmd, uint32_t* ctr,
+                                                       int64_t N, int64_t V, int K, int64_t seg,
+                                                       int64_t segs) {
+    // keys per lane the merge keeps in flight: as many as the region holds
+    constexpr int MB = (topk_region<T, U>() - region_slots(0)) / 64 < TK_MERGE_B
+                           ? (topk_region<T, U>() - region_slots(0)) / 64
+                           : TK_MERGE_B;
+    static_assert(MB >= 1, "merge fits the region");
+    __shared__ TopkSmem<T, U> sm;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int64_t vr = blockIdx.x;
+    if (lane < K) sm.region[wv][lane] = 0;
+    if (lane == 0) sm.published[wv] = 0;
+    __syncthreads();
+    if (!topk_vrow<T, 4, U, VAR, true, true>(sm, x, nullptr, nullptr, pkeys, pmd, V, K, seg, segs,
+                                             vr))
+        return;
+    // the partial's coherent stores have completed before the row's count moves
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const int64_t row = vr / segs;
+    uint32_t done = 0;
+    if (lane == 0)
+        done = __hip_atomic_fetch_add(ctr + row, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    done = __builtin_amdgcn_readfirstlane(done);
+    if (done != (uint32_t)segs - 1) return;
+    // every chunk of the row is in: its partials are read at the coherence
+    // point, after the count that says so
+    if (lane < K) sm.region[wv][lane] = 0;
+    topk_merge_row<VAR, true, MB>(sm.region[wv], pkeys, pmd, vals, idx, row, segs, K);
+    if (lane == 0) __hip_atomic_store(ctr + row, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // 16-byte vectors per lane per step, by shape and element type: enough
@@ -827,6 +937,11 @@ hipError_t launch_topk_t(const TopkLaunch& a) {
     uint64_t* pkeys = static_cast<uint64_t*>(a.part);
     MD* pmd = reinterpret_cast<MD*>(pkeys + a.N * a.S * a.K);
     dim3 grid((unsigned)(a.N * a.S));
+    if (a.ctr) {  // merge by each row's last chunk, in the same kernel
+        hipLaunchKernelGGL((topk_split1<T, topk_unroll<T, 4>(), VAR>), grid, block, 0, a.st, x,
+                           a.vals, a.idx, pkeys, pmd, a.ctr, a.N, a.V, a.K, a.chunk, a.S);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL((topk_fused<T, 4, topk_unroll<T, 4>(), VAR, true>), grid, block, 0, a.st,
                        x, nullptr, nullptr, pkeys, pmd, a.N, a.V, a.K, a.chunk, a.S);
     hipError_t e = hipGetLastError();

@@ -157,3 +157,30 @@ def test_workload_32768x128256_bf16_k50_sampled(dev):
     v64, z64 = oracle.topk(xh, w["K"], "bf16")
     assert_topk_equal(to_host(vals.index_select(0, rr)), to_host(idx.index_select(0, rr)),
                       v64, z64, "bf16 32768x128256 K=50 sample")
+
+
+def test_split_row_counters_reset(dev):
+    """Split top-k merges each row in the workgroup that completes it, counted
+    in a per-stream array that every call must leave cleared: back-to-back
+    calls with other batch sizes, chunk counts and K on one stream, then on a
+    second stream, each checked against the oracle."""
+    cases = [(10, 100003, 5, 7), (3, 50001, 9, 13), (10, 100003, 5, 7), (37, 20011, 64, 3),
+             (1, 200000, 1, 40), (10, 100003, 16, 2)]
+    xs = {c: synth.logits(c[0], c[1], sigma=2.0, seed=sum(c), device=dev) for c in cases}
+    s2 = torch.cuda.Stream()
+    for stream in (None, s2):
+        for c in cases:
+            N, V, K, S = c
+            print(f"split counters stream={'2nd' if stream else 'current'} N={N} V={V} K={K} S={S}",
+                  flush=True)
+            x = xs[c]
+            if stream is None:
+                vals, idx = osm.softmax_topk(x, K, kernel=osm.KERNEL_SPLIT, param=S)
+            else:
+                with torch.cuda.stream(stream):
+                    vals, idx = osm.softmax_topk(x, K, kernel=osm.KERNEL_SPLIT, param=S,
+                                                 stream=stream)
+                stream.synchronize()
+            torch.cuda.synchronize()
+            v64, z64 = oracle.topk(to_host(x), K, "f32")
+            assert_topk_equal(to_host(vals), to_host(idx), v64, z64, f"split counters {c}")
