@@ -181,6 +181,7 @@ H_, W_, O_ = 0x60000000, 0x70000000, 0x80000000
     (H_, W_, O_, -1, 64, 100),           # N < 0
     (H_, W_, O_, 4, 0, 100),             # H < 8
     (H_, W_, O_, 4, 60, 100),            # H not a multiple of 8
+    (H_, W_, O_, 4, (1 << 20) + 8, 100), # H above 2^20 (32-bit load offsets in a tile)
     (H_, W_, O_, 4, 64, 0),              # V < 1
     (H_, W_, O_, 65535 * 128 + 1, 64, 10),  # N above the grid limit
     (H_ + 2, W_, O_, 4, 64, 100),        # h not 16-byte aligned
@@ -204,6 +205,12 @@ def test_proj_fwd_rejects(args):
 ])
 def test_proj_softmax_topk_rejects(args):
     assert osm.lib().proj_softmax_topk(*args, None) == osm.EINVAL
+
+
+def test_proj_accepts_largest_h_without_launch():
+    """H = 2^20 passes the checks; N = 0 then returns OSM_OK without a launch."""
+    assert osm.lib().proj_fwd(H_, W_, O_, 0, 1 << 20, 100, None) == osm.OK
+    assert osm.lib().proj_softmax_topk(H_, W_, V_, I_, 0, 1 << 20, 100, 5, None) == osm.OK
 
 
 def test_proj_kmax_matches_header():
