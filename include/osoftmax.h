@@ -229,6 +229,17 @@ OSM_API int proj_fwd(const void* h, const void* w, float* logits, int64_t N, int
 OSM_API int proj_softmax_topk(const void* h, const void* w, float* vals, int32_t* idx,
                               int64_t N, int64_t H, int64_t V, int K, hipStream_t stream);
 
+/* Reference streaming kernels, for measurement only (nothing of the method):
+ * op 0 reads `bytes` bytes of x (y: a device buffer of at least 1 KB that
+ * the kernel may write, as a sink the compiler cannot remove); op 1 copies
+ * `bytes` bytes of x to y, with 16-byte non-temporal accesses: the
+ * plain read and copy rates against which the other kernels' bandwidth is
+ * judged.  x and y 16-byte aligned, bytes a multiple of 16, x and y not
+ * overlapping (op 1).  Each wavefront streams one contiguous span.
+ * Errors: OSM_EINVAL for another op, bytes < 0 or not
+ * a multiple of 16, null or misaligned pointers, overlap. */
+OSM_API int osm_ref_stream(int op, const void* x, void* y, int64_t bytes, hipStream_t stream);
+
 /* Kernel family and parameter softmax_fwd would use for this shape on the
  * current device (for OSM_RESIDENT: OSM_KERNEL_ROWS and the threads per row).  Errors: OSM_EINVAL for bad sizes, dtype or
  * null outputs; OSM_EUNSUPPORTED for OSM_RESIDENT rows it cannot hold. */

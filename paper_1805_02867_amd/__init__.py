@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
     L.proj_softmax_topk.restype = i32
     L.osm_plan.argtypes = [i64, i64, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i64)]
     L.osm_plan.restype = i32
+    L.osm_ref_stream.argtypes = [i32, vp, vp, i64, vp]
+    L.osm_ref_stream.restype = i32
     L.osm_status_string.argtypes = [i32]
     L.osm_status_string.restype = ctypes.c_char_p
     _lib = L
@@ -237,6 +239,22 @@ def _proj_inputs(h: torch.Tensor, w: torch.Tensor):
     if h.shape[1] != w.shape[1]:
         raise ValueError("h (N x H) and w (V x H) must have the same H")
     return h.shape[0], h.shape[1], w.shape[0]
+
+
+def ref_stream(op: str, x: torch.Tensor, y: torch.Tensor, stream=None) -> None:
+    """Reference streaming kernel for measurement (``osm_ref_stream``):
+    op "read" reads all of x (y: a sink of at least 1 KB), "copy" copies x
+    to y (same size).  Nothing of the method; the plain rates the other
+    kernels are judged against."""
+    if op not in ("read", "copy"):
+        raise ValueError("op must be 'read' or 'copy'")
+    n = x.numel() * x.element_size()
+    if op == "copy" and y.numel() * y.element_size() < n:
+        raise ValueError("y is smaller than x")
+    rc = lib().osm_ref_stream(0 if op == "read" else 1, x.data_ptr(), y.data_ptr(), n,
+                              _stream(stream))
+    if rc != OK:
+        raise OsmError(rc, "osm_ref_stream")
 
 
 def proj(h: torch.Tensor, w: torch.Tensor, out: torch.Tensor | None = None, stream=None):

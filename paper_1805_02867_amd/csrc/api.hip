@@ -510,6 +510,16 @@ int osm_topk_plan(int64_t N, int64_t V, int dtype, int K, int* kernel, int64_t* 
     return OSM_OK;
 }
 
+int osm_ref_stream(int op, const void* x, void* y, int64_t bytes, hipStream_t stream) {
+    if ((op != 0 && op != 1) || bytes < 0 || bytes % 16 != 0) return OSM_EINVAL;
+    if (bytes == 0) return OSM_OK;
+    if (!x || !y || !aligned(x, 16) || !aligned(y, 16)) return OSM_EINVAL;
+    if (op == 1 && overlaps(x, (size_t)bytes, y, (size_t)bytes)) return OSM_EINVAL;
+    DeviceState* ds = device_state(nullptr);
+    if (!ds) return OSM_EHIP;
+    return hip_status(osm::launch_ref_stream(op, x, y, bytes / 16, ds->cus, stream));
+}
+
 int proj_fwd(const void* h, const void* w, float* logits, int64_t N, int64_t H, int64_t V,
              hipStream_t stream) {
     return run_proj_logits(h, w, logits, N, H, V, stream);

@@ -40,6 +40,12 @@ hipError_t launch_proj_topk(const void* h, const void* w, float* vals, int32_t* 
                             void* part, int64_t N, int64_t H, int64_t V, int K, int64_t S,
                             int64_t tiles, int parts, hipStream_t st);
 
+// Reference streaming kernels (measurement only): op 0 reads `vecs` 16-byte
+// vectors of x (y: a 1 KB sink, written only for a sum never met), op 1
+// copies them to y.
+hipError_t launch_ref_stream(int op, const void* x, void* y, int64_t vecs, int cus,
+                             hipStream_t st);
+
 // What the top-k kernels compute next to the selection (Section 4, and the
 // comparisons of Section 5.2):
 //  TK_ONLINE: the online pair, one pass (Alg. 4);

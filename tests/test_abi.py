@@ -23,7 +23,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("softmax_fwd", "softmax_fwd_ex", "softmax_topk", "softmax_topk_dt",
                  "softmax_topk_ex", "softmax_topk_algo", "topk_fwd", "proj_fwd",
-                 "proj_softmax_topk", "osm_plan", "osm_topk_plan", "osm_status_string"):
+                 "proj_softmax_topk", "osm_plan", "osm_topk_plan", "osm_status_string",
+                 "osm_ref_stream"):
         assert want in names
 
 
@@ -248,3 +249,20 @@ def test_python_binding_refuses_cpu_tensors():
         osm.softmax_topk(torch.zeros(2, 3), 1)
     with pytest.raises(ValueError):
         osm.topk(torch.zeros(2, 3), 1)
+
+
+@pytest.mark.parametrize("args", [
+    (2, H_, W_, 1024),        # unknown op
+    (0, H_, W_, -16),         # negative size
+    (0, H_, W_, 1000),        # not a multiple of 16
+    (0, 0, W_, 1024),         # null x
+    (1, H_, 0, 1024),         # null y
+    (1, H_ + 4, W_, 1024),    # x not 16-byte aligned
+    (1, H_, H_ + 512, 1024),  # copy onto an overlapping y
+])
+def test_ref_stream_rejects(args):
+    assert osm.lib().osm_ref_stream(*args, None) == osm.EINVAL
+
+
+def test_ref_stream_empty_is_ok_without_launch():
+    assert osm.lib().osm_ref_stream(1, H_, W_, 0, None) == osm.OK

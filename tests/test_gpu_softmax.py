@@ -182,3 +182,15 @@ def test_workload_32768x128256_bf16_sampled(dev):
         xh = to_host(x.index_select(0, rr))
         yh = to_host(y.index_select(0, rr))
         assert_softmax_close(yh, oracle.softmax(xh, "bf16"), "bf16 32768x128256 sample")
+
+
+def test_ref_stream_copy_is_exact(dev):
+    """The reference copy kernel (a measurement aid) copies every byte, ragged
+    tail included; the read kernel runs on the same buffer."""
+    x = torch.randint(-2**31, 2**31 - 1, (1_000_003 * 4,), dtype=torch.int32, device=dev)
+    y = torch.empty_like(x)
+    osm.ref_stream("copy", x, y)
+    sink = torch.zeros(1024, dtype=torch.float32, device=dev)
+    osm.ref_stream("read", x, sink)
+    torch.cuda.synchronize()
+    assert torch.equal(x, y)
