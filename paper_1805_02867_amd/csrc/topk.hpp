@@ -450,7 +450,9 @@ __device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restric
     auto& wmd = sm.wmd;
     auto& wmx = sm.wmx;
     uint64_t* const published = sm.published;
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    // the wavefront index is uniform: taken as a scalar, so that the row, the
+    // step counts and every branch on them stay scalar
+    const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int rw = wv % W;                  // wavefront within the row
     const int tr = tid % TR;                // thread within the row
 
@@ -748,7 +750,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
                                                       int K, int64_t seg, int64_t segs) {
     constexpr int RB = TK_BLOCK / 64 / W;   // rows per workgroup
     __shared__ TopkSmem<T, U> sm;
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t vr = (int64_t)blockIdx.x * RB + wv / W;
     const bool live = vr < N * segs;        // uniform per wavefront (and per row)
     if (lane < K) sm.region[wv][lane] = 0;  // empty list
@@ -829,7 +831,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_merge(const uint64_t* __restric
     constexpr int WB = TK_BLOCK / 64;
     constexpr int REGION = region_slots(64 * TK_MERGE_B);
     __shared__ uint64_t region[WB][REGION];
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t row = (int64_t)blockIdx.x * WB + wv;
     if (lane < K) region[wv][lane] = 0;
     if (row >= N) return;
@@ -855,7 +857,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_split1(const T* __restrict__ x,
                            : TK_MERGE_B;
     static_assert(MB >= 1, "merge fits the region");
     __shared__ TopkSmem<T, U> sm;
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t vr = blockIdx.x;
     if (lane < K) sm.region[wv][lane] = 0;
     if (lane == 0) sm.published[wv] = 0;
@@ -893,6 +895,14 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_split1(const T* __restrict__ x,
 #ifndef OSM_TOPK_U4
 #define OSM_TOPK_U4 2
 #endif
+
+#ifndef OSM_TOPK_USPLIT
+#define OSM_TOPK_USPLIT 6
+#endif
+
+// The split kernels (a chunk per workgroup, for small batches) run only a
+// few workgroups per CU, so they can keep more loads in flight per lane.
+constexpr int topk_split_unroll() { return OSM_TOPK_USPLIT; }
 
 template <typename T, int W>
 constexpr int topk_unroll() {
@@ -938,11 +948,11 @@ hipError_t launch_topk_t(const TopkLaunch& a) {
     MD* pmd = reinterpret_cast<MD*>(pkeys + a.N * a.S * a.K);
     dim3 grid((unsigned)(a.N * a.S));
     if (a.ctr) {  // merge by each row's last chunk, in the same kernel
-        hipLaunchKernelGGL((topk_split1<T, topk_unroll<T, 4>(), VAR>), grid, block, 0, a.st, x,
+        hipLaunchKernelGGL((topk_split1<T, topk_split_unroll(), VAR>), grid, block, 0, a.st, x,
                            a.vals, a.idx, pkeys, pmd, a.ctr, a.N, a.V, a.K, a.chunk, a.S);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((topk_fused<T, 4, topk_unroll<T, 4>(), VAR, true>), grid, block, 0, a.st,
+    hipLaunchKernelGGL((topk_fused<T, 4, topk_split_unroll(), VAR, true>), grid, block, 0, a.st,
                        x, nullptr, nullptr, pkeys, pmd, a.N, a.V, a.K, a.chunk, a.S);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

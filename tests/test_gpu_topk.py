@@ -184,3 +184,25 @@ def test_split_row_counters_reset(dev):
             torch.cuda.synchronize()
             v64, z64 = oracle.topk(to_host(x), K, "f32")
             assert_topk_equal(to_host(vals), to_host(idx), v64, z64, f"split counters {c}")
+
+
+def test_split_merge_many_partials(dev):
+    """The merge seeds its list with the largest of the partials' first keys
+    for up to 256 partials per row and streams the rest: rows with more
+    partials than that, K on both sides of the round-selection limit (16),
+    chunks shorter than K (partials holding empty slots), and tied values."""
+    cases = [(2, 300000, 5, 600), (2, 300000, 64, 300), (3, 20000, 17, 400), (1, 500000, 1, 1000),
+             (5, 40000, 16, 257), (2, 65536, 64, 2048)]
+    g = torch.Generator(device=dev).manual_seed(21)
+    for N, V, K, S in cases:
+        print(f"split merge N={N} V={V} K={K} S={S}", flush=True)
+        x = synth.logits(N, V, sigma=2.0, seed=N * V + K, device=dev)
+        vals, idx = osm.softmax_topk(x, K, kernel=osm.KERNEL_SPLIT, param=S)
+        torch.cuda.synchronize()
+        v64, z64 = oracle.topk(to_host(x), K, "f32")
+        assert_topk_equal(to_host(vals), to_host(idx), v64, z64, f"split merge {N}x{V} K={K} S={S}")
+        t = torch.randint(-2, 3, (N, V), generator=g, device=dev).float()
+        vals, idx = osm.softmax_topk(t, K, kernel=osm.KERNEL_SPLIT, param=S)
+        torch.cuda.synchronize()
+        v64, z64 = oracle.topk(to_host(t), K, "f32")
+        assert_topk_equal(to_host(vals), to_host(idx), v64, z64, f"split merge ties {N}x{V} K={K} S={S}")
