@@ -283,12 +283,14 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
 }
 
 // Top-k plan: one wavefront per row once the batch alone can give every
-// SIMD several wavefronts; a small batch of long rows is split into chunks
-// (a workgroup each, about two workgroups per CU in all: every chunk pays a
-// fixed selection cost, so more, shorter chunks stop paying off early);
-// otherwise a workgroup (four wavefronts) per row.
+// SIMD several wavefronts, or when rows are short (up to 1536 elements: a
+// wavefront streams them in a step or two, and more wavefronts per row only
+// add the barrier and the cross-wavefront merge); a small batch of long rows
+// is split into chunks (a workgroup each, about two workgroups per CU in all:
+// every chunk pays a fixed selection cost, so more, shorter chunks stop
+// paying off early); otherwise a workgroup (four wavefronts) per row.
 Plan choose_topk(int64_t N, int64_t V, int cus) {
-    if (N >= 4 * (int64_t)cus) return {OSM_KERNEL_ROWS, 64};
+    if (N >= 4 * (int64_t)cus || V <= 1536) return {OSM_KERNEL_ROWS, 64};
     if (N < 2 * (int64_t)cus && V >= 8192) {
         int64_t S = (2 * (int64_t)cus + N - 1) / N;
         int64_t s_cap = V / 4096;  // keep chunks >= 4096 elements

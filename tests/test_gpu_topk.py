@@ -112,6 +112,8 @@ def test_deterministic(dev):
 def test_small_workload_16x1000(dev):
     w = synth.WORKLOADS["softmax_topk_16x1000_f32"]
     x = synth.logits(w["N"], w["V"], sigma=w["sigma"], seed=0, device=dev)
+    # short rows: one wavefront per row, whatever the batch size
+    assert osm.topk_plan(w["N"], w["V"], w["K"]) == (osm.KERNEL_ROWS, 64)
     check(x, w["K"], "16x1000 K=5")
 
 
