@@ -100,6 +100,27 @@ def queued_batches(fn, reps: int, batches: int, stream):
     return out
 
 
+def cold_calls(fn, reps: int, stream, flush):
+    """Per-call GPU time of `fn` with cold caches: before each call `flush()`
+    reads a buffer of at least 512 MB (twice the last-level cache) with
+    ordinary, cache-allocating loads: a read evicts the input without leaving
+    dirty lines whose write-back would land in the timed call, and
+    non-temporal loads would not evict it all.  Events bracket the call
+    alone; the calls are queued behind a spin kernel, as in queued_batches.
+    Returns one time (us) per call."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    torch.cuda._sleep(int(2.4e9 * 0.004))
+    for a, b in evs:
+        flush()
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) * 1e3 for a, b in evs]
+
+
 def proj_compare(osm, torch, N, H, V, K, reps, stream):
     """The projection (bfloat16 h: N x H, w: V x H) with softmax + top-K in its
     epilogue, against the two-kernel path (the same projection writing binary32
@@ -223,6 +244,11 @@ def sweep(path: str):
     cases.append(("sweep_4000x25000_f32", 4000, 25000, "f32", 2.0, {}))
     # accesses per element of each softmax + top-k algorithm (Section 4)
     algo_access = {"online_fused": 1, "safe_fused": 2, "online_unfused": 4, "safe_unfused": 5}
+    # inputs that fit in the 256 MB last-level cache are also timed cold
+    cold_mb = 256
+    scratch = torch.zeros(512 * 1024 * 1024 // 4, dtype=torch.float32, device="cuda")
+    sink = torch.empty(1024, dtype=torch.float32, device="cuda")
+    flush = lambda: torch.sum(scratch, dim=0, out=sink[:1].view(()))
     for name, N, V, dt, sg, extra in cases:
         x = synth.logits(N, V, sigma=sg, seed=0, dtype=dt, device="cuda", **extra)
         es = 2 if dt == "bf16" else 4
@@ -266,6 +292,22 @@ def sweep(path: str):
             emit({"workload": name, "op": f"topk_fused_k{K}", "N": N, "V": V, "dtype": dt,
                   "us": round(us, 2), "GBps": round((es * N * V + 8 * N * K) / us / 1e3, 1),
                   "elements_per_s": round(N * V / us * 1e6, 1), "rows_per_s": round(N / us * 1e6, 1)})
+        if es * N * V <= cold_mb * 1024 * 1024:
+            vals = torch.empty((N, 5), dtype=torch.float32, device="cuda")
+            idx = torch.empty((N, 5), dtype=torch.int32, device="cuda")
+            y = torch.empty_like(x)
+            for op, fn, nbytes in (
+                    ("softmax_online_cold", lambda: osm.softmax_fwd(x, y), 3 * es * N * V),
+                    ("topk_fused_k5_cold", lambda: osm.softmax_topk(x, 5, vals, idx),
+                     es * N * V + 40 * N)):
+                if op.startswith("topk") and V < 5:
+                    continue
+                fn()
+                us = median(cold_calls(fn, 20, stream, flush))
+                emit({"workload": name, "op": op, "N": N, "V": V, "dtype": dt,
+                      "us": round(us, 2), "GBps": round(nbytes / us / 1e3, 1),
+                      "elements_per_s": round(N * V / us * 1e6, 1)})
+            del y
         del x
         torch.cuda.empty_cache()
     for N, H, V in ((64, 4096, 128256), (512, 4096, 128256), (4000, 1024, 32000),
