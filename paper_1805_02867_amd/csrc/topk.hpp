@@ -409,20 +409,25 @@ __device__ __forceinline__ float sum_exp_fixed(float d, const float (&x)[N], flo
 // outputs (segs must be 1); PART = true writes, per virtual row, its K
 // largest keys (indices relative to the start of the row; 0 = fewer than K)
 // and its normalizer pair, which topk_merge combines.
-// LDS slots of one wavefront's list + queue region for a shape: the
-// candidate path checks the selection trigger after its first UH = U / 2
-// vectors and again at the end of the step, so at most max(UH, U - UH) * E
-// keys per lane are appended between two checks.
+// LDS slots of one wavefront's list + queue region for a shape: keys are
+// queued by the offer of a batch of candidate vectors (at most 64 E keys) or
+// of one scalar element per lane, each followed by a check of the selection
+// trigger.
 template <typename T, int U>
 constexpr int topk_region() {
-    constexpr int E = Vec<T>::N, UH = U / 2;
-    return region_slots(64 * E * (UH > U - UH ? UH : U - UH));
+    return region_slots(64 * Vec<T>::N);
 }
+
+// Candidate vectors waiting for their element-wise offer: at most 63 left
+// over from the last batch plus 64 appended before the next check.
+constexpr int TK_CV_CAP = 128;
 
 // The LDS of a workgroup of the fused top-k kernels.
 template <typename T, int U>
 struct TopkSmem {
     uint64_t region[TK_BLOCK / 64][topk_region<T, U>()];
+    u32x4 cvec[TK_BLOCK / 64][TK_CV_CAP];
+    uint32_t cidx[TK_BLOCK / 64][TK_CV_CAP];
     uint64_t published[TK_BLOCK / 64];
     MD wmd[TK_BLOCK / 64];
     float wmx[TK_BLOCK / 64];
@@ -445,7 +450,6 @@ __device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restric
     constexpr int E = Vec<T>::N;
     constexpr int TR = 64 * W;              // threads per row
     constexpr int64_t STEP = (int64_t)TR * U;
-    constexpr int UH = U / 2;
     auto& region = sm.region;
     auto& wmd = sm.wmd;
     auto& wmx = sm.wmx;
@@ -622,6 +626,51 @@ __device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restric
             if (kth != 0) tw.raise_tau((kth & 0xFFFFFFFF00000000ull) - 1);
         }
     };
+    // Candidate vectors.  A vector whose maximum reaches the threshold is
+    // appended whole (its 16 bytes and the index of its first element) to the
+    // wavefront's LDS list; each 64 of them are then offered element by
+    // element, one vector per lane, so that the per-element tests run on
+    // candidates in every lane instead of in the few lanes that hold one.
+    u32x4* const cvec = sm.cvec[wv];
+    uint32_t* const cidx = sm.cidx[wv];
+    int cn = 0;  // entries in the list (wave-uniform)
+    auto cv_drain = [&]() {  // offers the first min(cn, 64) entries
+        const int n = cn < 64 ? cn : 64;
+        const bool has = lane < n;
+        wave_sync();
+        const u32x4 q = cvec[has ? lane : 0];
+        const uint32_t i0 = cidx[has ? lane : 0];
+        const int m = cn - n;  // left over, moved to the front
+        u32x4 r = q;
+        uint32_t ri = 0;
+        if (lane < m) {
+            r = cvec[64 + lane];
+            ri = cidx[64 + lane];
+        }
+        wave_sync();
+        if (lane < m) {
+            cvec[lane] = r;
+            cidx[lane] = ri;
+        }
+        cn = m;
+        float xv[E];
+        widen<T>(has ? q : ninf, xv);
+        tw.template offer<E>(xv, base + i0, has);
+        if (tw.qcount >= fa) tw.flush();
+    };
+    auto cv_append = [&](bool p, const u32x4& q, uint32_t i0) {
+        const uint64_t mask = __builtin_amdgcn_ballot_w64(p);
+        if (mask == 0) return;
+        const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+            (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+        if (p) {
+            cvec[cn + below] = q;
+            cidx[cn + below] = i0;
+        }
+        cn += __builtin_popcountll(mask);
+        if (cn >= 64) cv_drain();
+    };
+
     // One step: the lane's maximum over the step (one rescale test, and one
     // candidate test, per step), the exponentials of every element, then the
     // vectors that may hold a candidate are offered.
@@ -646,14 +695,10 @@ __device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restric
             for (int u = 0; u < U; ++u) {
                 float xv[E];
                 widen<T>(masked && !ok[u] ? ninf : buf[u], xv);
-                if (__builtin_amdgcn_ballot_w64(ok[u] && vec_max(xv) >= tw.tau_v) != 0) {
-                    const int64_t e0 = head + (b0 + (int64_t)u * TR + tr) * E;
-                    tw.template offer<E>(xv, base + (uint32_t)e0, ok[u]);
-                }
-                if (UH > 0 && u == UH - 1 && tw.qcount >= fa) tw.flush();
+                const uint32_t e0 = (uint32_t)(head + (b0 + (int64_t)u * TR + tr) * E);
+                cv_append(ok[u] && vec_max(xv) >= tw.tau_v, buf[u], e0);
             }
         }
-        if (tw.qcount >= fa) tw.flush();
         tw.pull();
     };
 
@@ -690,6 +735,7 @@ __device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restric
         }
         step(bt, ok, b0, true);
     }
+    while (cn > 0) cv_drain();
     tw.flush();
 
     // merge of the normalizer pairs: wavefront butterflies, then (W > 1)
