@@ -63,7 +63,10 @@ constexpr int TK_KMAX = 64;            // largest supported K (one list slot per
 constexpr int TK_FLUSH_MAX = 64;       // largest selection trigger (queued keys)
 constexpr int TK_PER_LANE = 5;         // rows of 64 slots per K-round selection block
 // Selections with more than this many rounds use the sorting network.
-constexpr int TK_ROUNDS_MAX = 16;
+#ifndef OSM_TOPK_ROUNDS_MAX
+#define OSM_TOPK_ROUNDS_MAX 8
+#endif
+constexpr int TK_ROUNDS_MAX = OSM_TOPK_ROUNDS_MAX;
 
 // Select early once the queue holds this many (per K): a threshold refreshed
 // often saves candidates; the K-round selection costs K rounds, so its
