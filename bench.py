@@ -198,6 +198,22 @@ def proj_probe(osm):
     log("proj probe done")
 
 
+def topk_probe(osm, synth):
+    """The fused softmax + top-k at 4000 x 32000 binary32 (K = 5, 50) and
+    32768 x 128256 bfloat16 (K = 5, 50), three calls each, for kernel
+    statistics and counters under a profiler."""
+    import torch
+    for N, V, dt, sg in ((4000, 32000, "f32", 2.0), (32768, 128256, "bf16", 4.0)):
+        x = synth.logits(N, V, sigma=sg, seed=0, dtype=dt, device="cuda")
+        for K in (5, 50):
+            for _ in range(3):
+                osm.softmax_topk(x, K)
+        torch.cuda.synchronize()
+        del x
+        torch.cuda.empty_cache()
+    log("topk probe done")
+
+
 def sweep(path: str):
     """Every workload shape, the paper's V sweeps at batch 4000 and 10, and
     its K sweep: one JSON record per (shape, op) into `path`.  Each record is
@@ -325,6 +341,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--proj-probe", action="store_true")
+    ap.add_argument("--topk-probe", action="store_true")
     ap.add_argument("--compare-reps", type=int, default=20)
     ap.add_argument("--sweep", metavar="FILE", help="time every workload shape and the V "
                     "sweeps; one JSON record per line into FILE")
@@ -347,6 +364,9 @@ def main():
         return
     if args.proj_probe:
         proj_probe(osm)
+        return
+    if args.topk_probe:
+        topk_probe(osm, synth)
         return
     if args.sweep:
         sweep(args.sweep)
