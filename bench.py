@@ -69,6 +69,17 @@ def traffic_entry(name: str):
     return e.get("bytes_per_launch")
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (Linux), or an empty string."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
 def timed_calls(fn, reps: int, stream):
     import torch
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -482,7 +493,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        rows = N  # the whole batch: about 10 s of CPU work on 16 cores
+        rows = N  # the whole batch: about 10-15 core-seconds
         xh = x[:rows].cpu().numpy()
         oracle.softmax(xh[:8])  # load the library outside the timing
         t1 = time.perf_counter()
@@ -490,11 +501,26 @@ def main():
         oracle.topk(xh, K)
         dt = time.perf_counter() - t1
         cpu_bytes = rows * V * 12.0 + rows * V * 4.0 + rows * K * 8.0
+        threads = oracle.threads()
+        # the same work on one core, on a smaller sample
+        rows1 = 250
+        oracle.set_threads(1)
+        t1 = time.perf_counter()
+        oracle.softmax(xh[:rows1])
+        oracle.topk(xh[:rows1], K)
+        dt1 = time.perf_counter() - t1
+        oracle.set_threads(threads)
         cpu = {"value": round(cpu_bytes / dt / 1e9, 3), "unit": "GB/s",
-               "cores": oracle.threads(), "kind": "oracle",
+               "cores": threads, "kind": "oracle",
                "sample": f"{rows} of the {N} rows (the whole batch), one step: softmax "
-                         f"(Eq. 2, all rows) + top-5 by full sort, {dt:.2f} s wall"}
-        log(f"oracle: {dt:.2f} s for {rows} rows on {oracle.threads()} threads")
+                         f"(Eq. 2, all rows) + top-5 by full sort, {dt:.2f} s wall",
+               "rows_per_s": round(rows / dt, 1), "elements_per_s": round(rows * V / dt, 1),
+               "cpu_model": cpu_model(), "nproc": len(os.sched_getaffinity(0)),
+               "one_core": {"rows_per_s": round(rows1 / dt1, 1),
+                            "elements_per_s": round(rows1 * V / dt1, 1),
+                            "sample": f"{rows1} rows, {dt1:.2f} s wall"}}
+        log(f"oracle: {dt:.2f} s for {rows} rows on {threads} threads; "
+            f"{dt1:.2f} s for {rows1} rows on one")
 
     out = {
         "metric": "achieved HBM GB/s (% of peak) for online softmax + fused softmax+top-K rows/s",
