@@ -116,30 +116,49 @@ __device__ __forceinline__ void pj_dma(uint16_t (&tile)[ROWS][PJ_BK], __amdgpu_b
     }
 }
 
-// The 16-byte fragment of row r, chunk kc of a tile.
+// Byte offsets, within a tile, of a lane's fragment reads for the blocks of
+// a wavefront whose first row is `base` (a multiple of 32): sub-step ks of
+// block m reads row base + 32 m + l % 32, chunk 2 ks + l / 32, at byte
+// off[ks] + 4096 m.  The row adds a multiple of 16 to (row / 2) for every m,
+// so the slot's XOR term is (l % 32) / 2 % 8 for all blocks: one offset per
+// sub-step, and the block's part is an instruction offset.
+template <int KS>
+struct PjFragOff {
+    uint32_t off[KS];
+    __device__ __forceinline__ static PjFragOff make(int base) {
+        const int lane = threadIdx.x & 63, lr = lane & 31, lh = lane >> 5;
+        PjFragOff f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            f.off[ks] = (uint32_t)((base + lr) * PJ_BK * 2 + 16 * pj_slot(lr, 2 * ks + lh));
+        return f;
+    }
+};
+
 template <int ROWS>
-__device__ __forceinline__ bf16x8 pj_frag(const uint16_t (&tile)[ROWS][PJ_BK], int r, int kc) {
-    return __builtin_bit_cast(
-        bf16x8, *reinterpret_cast<const u32x4*>(&tile[r][pj_slot(r, kc) * 8]));
+__device__ __forceinline__ bf16x8 pj_frag(const uint16_t (&tile)[ROWS][PJ_BK], uint32_t off,
+                                          int m) {
+    const char* p = reinterpret_cast<const char*>(&tile[0][0]) + off + m * 32 * PJ_BK * 2;
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
 }
 
 // acc[mi][ni] += the wavefront's (32 MI) x (32 NI) block of X-tile . Y-tile^T
-// over one K step; the block starts at row bx of the X tile and row by of the
-// Y tile.  The fragments of sub-step ks + 1 are read into the other register
-// set before the products of sub-step ks are issued.
+// over one K step; the block starts at the X-tile row and Y-tile row whose
+// fragment offsets are xo and yo.  The fragments of sub-step ks + 1 are read
+// into the other register set before the products of sub-step ks are issued.
 template <class C>
 __device__ __forceinline__ void pj_mma(const uint16_t (&xt)[C::TX][PJ_BK],
-                                       const uint16_t (&yt)[C::TY][PJ_BK], int bx, int by,
+                                       const uint16_t (&yt)[C::TY][PJ_BK],
+                                       const PjFragOff<PJ_BK / 16>& xo,
+                                       const PjFragOff<PJ_BK / 16>& yo,
                                        f32x16 (&acc)[C::MI][C::NI]) {
     constexpr int MI = C::MI, NI = C::NI, KS = PJ_BK / 16;
-    const int lane = threadIdx.x & 63;
-    const int lr = lane & 31, lh = lane >> 5;
     bf16x8 a[2][MI], b[2][NI];  // [register set][block]
     auto read = [&](int set, int ks) {
 #pragma unroll
-        for (int mi = 0; mi < MI; ++mi) a[set][mi] = pj_frag(xt, bx + mi * 32 + lr, 2 * ks + lh);
+        for (int mi = 0; mi < MI; ++mi) a[set][mi] = pj_frag(xt, xo.off[ks], mi);
 #pragma unroll
-        for (int ni = 0; ni < NI; ++ni) b[set][ni] = pj_frag(yt, by + ni * 32 + lr, 2 * ks + lh);
+        for (int ni = 0; ni < NI; ++ni) b[set][ni] = pj_frag(yt, yo.off[ks], ni);
     };
     read(0, 0);
 #pragma unroll
@@ -203,6 +222,8 @@ __device__ __forceinline__ void pj_run(const uint16_t* __restrict__ X, int64_t n
                                        Coords&& coords, Epi&& epi) {
     const int wave = pj_wave();
     const int bx = (wave / C::WY) * 32 * C::MI, by = (wave % C::WY) * 32 * C::NI;
+    const PjFragOff<PJ_BK / 16> xo = PjFragOff<PJ_BK / 16>::make(bx),
+                                yo = PjFragOff<PJ_BK / 16>::make(by);
     const PjAddr a = PjAddr::make<C>(K);
     const int64_t nk = pj_steps(K);
     int64_t x0, y0;
@@ -224,11 +245,11 @@ __device__ __forceinline__ void pj_run(const uint16_t* __restrict__ X, int64_t n
         for (int64_t k = 0; k < nk; k += 2) {
             pj_handover();
             pj_issue<C>(sm, 1, rx, ry, a, K, k + 1);
-            pj_mma<C>(sm.st[0].x, sm.st[0].y, bx, by, acc);
+            pj_mma<C>(sm.st[0].x, sm.st[0].y, xo, yo, acc);
             pj_handover();
             if (k + 2 < nk) pj_issue<C>(sm, 0, rx, ry, a, K, k + 2);
             else if (more) pj_issue<C>(sm, 0, rxn, ryn, a, K, 0);
-            pj_mma<C>(sm.st[1].x, sm.st[1].y, bx, by, acc);
+            pj_mma<C>(sm.st[1].x, sm.st[1].y, xo, yo, acc);
         }
         // every wavefront's last read of stage 1 is done before epi may write it
         __builtin_amdgcn_s_barrier();

@@ -3,17 +3,17 @@
 // that the logits never leave the chip (the Discussion's proposal).
 //
 // Fused kernel.  Workgroup (c, b) computes P = W . h^T for the vocabulary
-// tiles of chunk c against batch rows [256 b, 256 b + 256): with W as the
-// MFMA's A operand, each lane's result registers hold, per tile, 128
-// vocabulary entries of each of two batch rows (columns of P), so a lane
-// keeps, for each of those rows,
+// tiles of chunk c against a strip of batch rows: with W as the MFMA's A
+// operand, each lane's result registers hold, per tile, a run of vocabulary
+// entries of each of its batch rows (columns of P), so a lane keeps, for each
+// of those rows,
 //  * the online pair (s, d) of the entries it has seen (Alg. 3's update,
 //    with the reference moved only when the tile maximum passes it by more
 //    than kLazy, as in the other one-pass kernels), and
 //  * its own sorted list of the K largest keys it has seen (Alg. 4's buffer),
 //    entered only by values at or above the list's K-th value.
-// The two holders of a batch row in a workgroup (the two lane halves) each
-// write their pair and list as a partial;
+// Every holder of a batch row in a workgroup (two lane halves in each
+// wavefront along the vocabulary) writes its pair and list as a partial;
 // the split top-k merge kernel combines a row's partials (Eq. 4 for the
 // pairs, the key order for the lists).
 #include "proj.hpp"
@@ -26,18 +26,28 @@ namespace osm {
 // per CU), which keep small problems spread over more CUs.
 using PjBig = PjCfg<256, 256, 2, 4>;
 using PjSmall = PjCfg<128, 128, 2, 2>;
-// Fused, by batch size and K (the vocabulary tile is 256 entries in all):
-//  * 256 x 256 (K <= 8, N > 128): four wavefronts side by side along the
-//    batch, two batch rows per lane, the lanes' top-K lists in the 32 KB of
-//    LDS beside the two stages (the core takes the registers);
-//  * 256 x 128 (otherwise, N > 64): one batch row per lane, lists in
-//    registers;
+// Fused, by batch size and K (the vocabulary tile is 256 entries in all; the
+// lanes' top-K lists live in registers):
+//  * 256 x 256 (K <= 8, N > 128): 2 x 4 wavefronts, two batch rows per lane;
+//    128 result registers and at most 128 others per lane, so two
+//    wavefronts share each SIMD and one's epilogue overlaps the other's
+//    products;
+//  * 256 x 128 in 2 x 4 wavefronts (8 < K <= 16, N > 1024): one batch row per
+//    lane, also two wavefronts per SIMD;
+//  * 256 x 128 in 1 x 4 wavefronts (otherwise, N > 64): one batch row per
+//    lane, one wavefront per SIMD, measured faster than the 2 x 4 layout up
+//    to N = 512;
 //  * 256 x 64 (N <= 64): 2 x 2 wavefronts, one batch row per lane, so small
 //    batches do not pay for a strip of 256 rows.
-using PjFused8 = PjCfg<256, 256, 1, 4>;
+using PjFused8 = PjCfg<256, 256, 2, 4>;
+using PjFused16W = PjCfg<256, 128, 2, 4>;
 using PjFused16 = PjCfg<256, 128, 1, 4>;
 using PjFusedN = PjCfg<256, 64, 2, 2>;
-static int fused_cfg(int64_t N, int K) { return N <= 64 ? 2 : (K <= 8 && N > 128 ? 0 : 1); }
+static int fused_cfg(int64_t N, int K) {
+    if (N <= 64) return 3;
+    if (K <= 8 && N > 128) return 0;
+    return K > 8 && N > 1024 ? 1 : 2;
+}
 
 // ------------------------------------------------------------ plain logits
 // Tiles in grouped order: groups of up to 8 batch strips, each taken across
@@ -130,63 +140,42 @@ __device__ __forceinline__ uint32_t below_bit(float x, float t, int j) {
     return (__float_as_uint(x - t) >> 31) << j;
 }
 
-// A lane's top-K list (descending keys, K valid, unused entries 0): KC
-// registers, or KC words of LDS (thread t's entry i at word i * NT + t).
-template <int KC, bool LDS>
-struct LaneList;
+// A lane's top-K list: KC registers of descending keys, K valid, unused
+// entries 0.
 template <int KC>
-struct LaneList<KC, false> {
+struct LaneList {
     uint64_t L[KC];
-    __device__ __forceinline__ void init(uint64_t*) {
+    __device__ __forceinline__ void init() {
 #pragma unroll
         for (int i = 0; i < KC; ++i) L[i] = 0ull;
     }
     // insert (key > K-th entry); returns the new K-th entry
-    __device__ __forceinline__ uint64_t insert(uint64_t*, int K, uint64_t key) {
+    __device__ __forceinline__ uint64_t insert(int K, uint64_t key) {
         list_insert<KC>(L, K, key);
         return list_kth<KC>(L, K);
     }
-    __device__ __forceinline__ uint64_t get(const uint64_t*, int i) const { return L[i]; }
-};
-template <int KC>
-struct LaneList<KC, true> {
-    static constexpr int NT = 256;  // threads of the workgroup (the column stride)
-    __device__ __forceinline__ void init(uint64_t* m) {
-#pragma unroll
-        for (int i = 0; i < KC; ++i) m[i * NT] = 0ull;
-    }
-    __device__ __forceinline__ uint64_t insert(uint64_t* m, int K, uint64_t key) {
-        uint64_t L[KC];
-#pragma unroll
-        for (int i = 0; i < KC; ++i) L[i] = m[i * NT];
-        list_insert<KC>(L, K, key);
-#pragma unroll
-        for (int i = 0; i < KC; ++i) m[i * NT] = L[i];
-        return list_kth<KC>(L, K);
-    }
-    __device__ __forceinline__ uint64_t get(const uint64_t* m, int i) const { return m[i * NT]; }
 };
 
 // One chunk of vocabulary tiles [c * tiles, min((c + 1) * tiles, nt)) for one
-// batch strip of TY rows.  Lane l of wavefront w holds, for batch rows
-// (TY / 4) w + 32 ni + l % 32 (ni < NI) of the strip, the entries
-// vbase + 32 mi + 8 (i / 4) + i % 4 (vbase = tile start + 4 (l / 32), mi < 8)
-// in result register i of block (mi, ni).  The partial of a (row, chunk) pair
-// written by this lane is p = 2 c + l / 32: 2 S per row, each a pair and K
-// keys (0 = none).
-template <class C, int KC, bool LDSL>
+// batch strip of TY rows.  Lane l of wavefront (wx, wy) holds, for batch rows
+// 32 (NI wy + ni) + l % 32 (ni < NI) of the strip, the entries
+// vbase + 32 mi + 8 (i / 4) + i % 4 (vbase = tile start + 32 MI wx + 4 (l / 32),
+// mi < MI) in result register i of block (mi, ni).  The partial of a (row, chunk) pair
+// written by this lane is p = 2 (WX c + wx) + l / 32: 2 WX S per row, each a
+// pair and K keys (0 = none).
+template <class C, int KC>
 __global__ __launch_bounds__(C::NT) void proj_topk_part(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, uint64_t* __restrict__ pkeys,
     MD* __restrict__ pmd, int64_t N, int64_t H, int64_t V, int K, int64_t S, int64_t tiles,
     int64_t per) {
-    static_assert(!LDSL || C::NT == 256, "LDS lists are laid out for 256 threads");
     constexpr int NI = C::NI;
     constexpr int E = C::MI * 16;  // entries per row per lane and tile
     // entries per pass of the LDS column: the largest power of two that fits a stage
-    constexpr int EC = sizeof(typename C::Stage) >= C::NT * 64 * sizeof(float) ? 64 : 32;
+    constexpr int EC = sizeof(typename C::Stage) >= C::NT * 64 * sizeof(float)   ? 64
+                       : sizeof(typename C::Stage) >= C::NT * 32 * sizeof(float) ? 32
+                                                                                 : 16;
     static_assert(sizeof(typename C::Stage) >= C::NT * EC * sizeof(float), "scratch fits");
     __shared__ typename C::Smem sm;
-    __shared__ uint64_t lists[LDSL ? NI * KC * C::NT : 1];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wx = wave / C::WY, wy = wave % C::WY;
     // Logical ids in blocks of PJ_CB chunks x up to PJ_SB batch strips, so
@@ -206,16 +195,14 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
 
     float sr[NI], dacc[NI], tval[NI];
     uint64_t tkey[NI];  // K-th key of the list (0 while it has fewer)
-    LaneList<KC, LDSL> list[NI];
-    uint64_t* lmem[NI];
+    LaneList<KC> list[NI];
 #pragma unroll
     for (int ni = 0; ni < NI; ++ni) {
         sr[ni] = kEmptyS;
         dacc[ni] = 0.0f;
         tval[ni] = -__builtin_inff();
         tkey[ni] = 0ull;
-        lmem[ni] = lists + (LDSL ? ni * KC * C::NT + threadIdx.x : 0);
-        list[ni].init(lmem[ni]);
+        list[ni].init();
     }
     float* scr = reinterpret_cast<float*>(&sm.st[1]) + threadIdx.x;  // this thread's column
 
@@ -235,7 +222,7 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
             auto offer = [&](int ni, float xv, int j) {
                 const uint64_t key = make_key(xv, (uint32_t)(vbase + voff(j)));
                 if (key > tkey[ni]) {
-                    tkey[ni] = list[ni].insert(lmem[ni], K, key);
+                    tkey[ni] = list[ni].insert(K, key);
                     // until the list holds K keys the threshold stays as it is
                     if (tkey[ni] != 0) tval[ni] = key_value(tkey[ni]);
                 }
@@ -335,8 +322,13 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
 #pragma unroll
                 for (int q = 0; q < E / EC; ++q) {
                     uint64_t m = 0;  // candidates of this part
+                    if constexpr (EC >= 32) {
 #pragma unroll
-                    for (int u = 0; u < EC / 32; ++u) m |= (uint64_t)~cm[q * (EC / 32) + u] << (32 * u);
+                        for (int u = 0; u < EC / 32; ++u)
+                            m |= (uint64_t)~cm[q * (EC / 32) + u] << (32 * u);
+                    } else {
+                        m = (~cm[q * EC / 32] >> (q * EC % 32)) & ((1u << EC) - 1u);
+                    }
                     if (!recompute && !remask && __builtin_amdgcn_ballot_w64(m != 0) == 0) continue;
                     stage(ni, q);
                     if (recompute || remask) {
@@ -380,7 +372,7 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
             uint64_t* dst = pkeys + (row * Sp + p) * K;
 #pragma unroll
             for (int i = 0; i < KC; ++i)
-                if (i < K) dst[i] = list[ni].get(lmem[ni], i);
+                if (i < K) dst[i] = list[ni].L[i];
             pmd[row * Sp + p] = MD{sr[ni], dacc[ni]};
         }
     }
@@ -407,9 +399,15 @@ hipError_t launch_proj_logits(const void* h, const void* w, float* out, int64_t 
 void proj_topk_shape(int64_t N, int64_t V, int K, int cus, int64_t* S, int64_t* tiles,
                      int* parts) {
     const int cfg = fused_cfg(N, K);
-    const int64_t TY = cfg == 0 ? PjFused8::TY : cfg == 1 ? PjFused16::TY : PjFusedN::TY;
+    const int64_t TY = cfg == 0 ? PjFused8::TY
+                       : cfg == 1 ? PjFused16W::TY
+                       : cfg == 2 ? PjFused16::TY
+                                  : PjFusedN::TY;
     const int64_t TX = PjFused8::TX;
-    *parts = 2 * (cfg == 0 ? PjFused8::WX : cfg == 1 ? PjFused16::WX : PjFusedN::WX);
+    *parts = 2 * (cfg == 0 ? PjFused8::WX
+                  : cfg == 1 ? PjFused16W::WX
+                  : cfg == 2 ? PjFused16::WX
+                             : PjFusedN::WX);
     // vocabulary chunks: about one workgroup per CU in all (each takes 80 KB
     // of LDS or more)
     const int64_t nb = (N + TY - 1) / TY, nt = (V + TX - 1) / TX;
@@ -425,14 +423,14 @@ size_t proj_topk_part_bytes(int64_t N, int64_t S, int parts, int K) {
     return (size_t)N * (size_t)(S * parts) * ((size_t)K * 8 + 8);
 }
 
-template <class C, int KC, bool LDSL>
+template <class C, int KC>
 static void launch_part(const void* h, const void* w, uint64_t* pkeys, MD* pmd, int64_t N,
                         int64_t H, int64_t V, int K, int64_t S, int64_t tiles, hipStream_t st) {
     const int64_t nb = (N + C::TY - 1) / C::TY;
     const int64_t sb = nb < PJ_SB ? nb : PJ_SB, nsb = (nb + sb - 1) / sb;
     const int64_t ids = (S + PJ_CB - 1) / PJ_CB * nsb * PJ_CB * sb;  // whole blocks
     const int64_t per = (ids + 7) / 8;
-    hipLaunchKernelGGL((proj_topk_part<C, KC, LDSL>), dim3((unsigned)(8 * per)), dim3(C::NT), 0,
+    hipLaunchKernelGGL((proj_topk_part<C, KC>), dim3((unsigned)(8 * per)), dim3(C::NT), 0,
                        st, (const uint16_t*)h, (const uint16_t*)w, pkeys, pmd, N, H, V, K, S,
                        tiles, per);
 }
@@ -445,11 +443,13 @@ hipError_t launch_proj_topk(const void* h, const void* w, float* vals, int32_t* 
     MD* pmd = reinterpret_cast<MD*>(pkeys + N * Sp * K);
     const int cfg = fused_cfg(N, K);
     if (cfg == 0)
-        launch_part<PjFused8, 8, true>(h, w, pkeys, pmd, N, H, V, K, S, tiles, st);
+        launch_part<PjFused8, 8>(h, w, pkeys, pmd, N, H, V, K, S, tiles, st);
     else if (cfg == 1)
-        launch_part<PjFused16, 16, false>(h, w, pkeys, pmd, N, H, V, K, S, tiles, st);
+        launch_part<PjFused16W, 16>(h, w, pkeys, pmd, N, H, V, K, S, tiles, st);
+    else if (cfg == 2)
+        launch_part<PjFused16, 16>(h, w, pkeys, pmd, N, H, V, K, S, tiles, st);
     else
-        launch_part<PjFusedN, 16, false>(h, w, pkeys, pmd, N, H, V, K, S, tiles, st);
+        launch_part<PjFusedN, 16>(h, w, pkeys, pmd, N, H, V, K, S, tiles, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     constexpr int WB = TK_BLOCK / 64;

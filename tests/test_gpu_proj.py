@@ -97,7 +97,7 @@ def test_proj_topk_exact(dev, N, H, V, K):
 
 
 @pytest.mark.parametrize("N,H,V,K", [(64, 512, 3000, 5), (257, 1024, 8000, 10),
-                                     (16, 256, 32000, 16)])
+                                     (16, 256, 32000, 16), (1100, 256, 5000, 12)])
 def test_proj_topk_random(dev, N, H, V, K):
     """Indices: where the oracle's K-th and (K+1)-th logits are further apart
     than twice the bound, the GPU must return exactly the oracle's indices;
@@ -149,12 +149,13 @@ def test_proj_topk_all_equal_logits(dev, K):
     assert_softmax_close(to_host(vals), np.full((N, K), 1.0 / V), "all-equal logits")
 
 
-@pytest.mark.parametrize("N", [64, 65, 128, 129, 257])
+@pytest.mark.parametrize("N", [64, 65, 128, 129, 257, 1024, 1025])
 @pytest.mark.parametrize("K", [5, 9, 16])
 def test_proj_topk_tile_shapes(dev, N, K):
-    """Batch sizes on each side of the fused kernel's tile choices (256 x 64,
-    256 x 128 and 256 x 256 tiles), with a ragged last vocabulary tile and a
-    K that is not a multiple of the 64-element step."""
+    """Batch sizes on each side of the fused kernel's tile and layout choices
+    (256 x 64, 256 x 128 in one or two wavefronts along the vocabulary, and
+    256 x 256 tiles), with a ragged last vocabulary tile and a K that is not a
+    multiple of the 64-element step."""
     H, V = 136, 3001
     h, w = exact_inputs(N, H, V, seed=N * 31 + K, dev=dev)
     vals, idx = osm.proj_softmax_topk(h, w, K)
