@@ -214,7 +214,11 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
         },
         [&](int64_t, int64_t x0, int64_t, f32x16 (&acc)[C::MI][C::NI]) {
             constexpr int E = C::MI * 16;  // entries per row per lane
-            constexpr int NG = E / 8;      // groups of 8 entries
+            // groups of GS consecutive entries: 8, or fewer so that there
+            // are at least KC groups (the bootstrap below needs K of them)
+            constexpr int GS = E / KC < 8 ? E / KC : 8;
+            constexpr int NG = E / GS;
+            static_assert(GS % 2 == 0 && NG >= KC, "groups hold whole entry pairs");
             const int64_t vbase = x0 + wx * 32 * C::MI + 4 * (lane >> 5);
             // offset from vbase of entry j (block j / 16, register j % 16)
             auto voff = [](int j) { return (j >> 4) * 32 + 8 * ((j & 15) >> 2) + (j & 3); };
@@ -240,7 +244,7 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni) {
                 // 1. One pass over the row's entries (the only code unrolled
-                //    over them): the maxima of groups of 8, the terms against
+                //    over them): the maxima of groups of GS, the terms against
                 //    the current reference and the entries below the list's
                 //    K-th value (tval only rises, so every entry that can still
                 //    enter the list is outside that set).
@@ -257,7 +261,7 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
                     for (int j = 0; j < E; j += 2) {
                         const float a0 = acc_reread(acc[j >> 4][ni][j & 15]);
                         const float a1 = acc_reread(acc[(j + 1) >> 4][ni][(j + 1) & 15]);
-                        bm[j >> 3] = max3_raw(bm[j >> 3], a0, a1);
+                        bm[j / GS] = max3_raw(bm[j / GS], a0, a1);
                         dsum[j & 3] += exp2_hw(__builtin_fmaf(a0, kLog2e, -sr[ni]));
                         dsum[(j + 1) & 3] += exp2_hw(__builtin_fmaf(a1, kLog2e, -sr[ni]));
                         cm[j >> 5] |= below_bit(a0, th, j & 31) | below_bit(a1, th, (j + 1) & 31);
@@ -266,7 +270,7 @@ __global__ __launch_bounds__(C::NT) void proj_topk_part(
 #pragma unroll
                     for (int j = 0; j < E; ++j) {
                         const float a = acc_reread(acc[j >> 4][ni][j & 15]);
-                        bm[j >> 3] = __builtin_fmaxf(bm[j >> 3], voff(j) < lim ? a : -__builtin_inff());
+                        bm[j / GS] = __builtin_fmaxf(bm[j / GS], voff(j) < lim ? a : -__builtin_inff());
                     }
                 }
                 float lm = bm[0];
