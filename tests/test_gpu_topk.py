@@ -7,7 +7,7 @@ import torch
 import oracle
 import paper_1805_02867_amd as osm
 from paper_1805_02867_amd import synth
-from parity import assert_topk_equal, host_dtype, to_host
+from parity import assert_softmax_close, assert_topk_equal, host_dtype, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -186,6 +186,38 @@ def test_split_row_counters_reset(dev):
             torch.cuda.synchronize()
             v64, z64 = oracle.topk(to_host(x), K, "f32")
             assert_topk_equal(to_host(vals), to_host(idx), v64, z64, f"split counters {c}")
+
+
+def test_split_calls_on_two_streams_at_once(dev):
+    """Split top-k and split softmax enqueued alternately on two streams with
+    no synchronisation between the calls: each stream has its own scratch and
+    row counters, so every result must match the oracle."""
+    cases = [(10, 100003, 5, 7), (3, 50001, 9, 13), (6, 30011, 64, 5)]
+    xs = [synth.logits(N, V, sigma=2.0, seed=300 + i, device=dev)
+          for i, (N, V, K, S) in enumerate(cases)]
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    for rep in range(3):
+        for i, (N, V, K, S) in enumerate(cases):
+            s = sa if (rep + i) % 2 == 0 else sb
+            print(f"two streams rep={rep} case={cases[i]}", flush=True)
+            with torch.cuda.stream(s):
+                vals, idx = osm.softmax_topk(xs[i], K, kernel=osm.KERNEL_SPLIT, param=S, stream=s)
+                y = osm.softmax_fwd(xs[i], kernel=osm.KERNEL_SPLIT, param=S, stream=s)
+            outs.append((i, vals, idx, y))
+    sa.synchronize()
+    sb.synchronize()
+    torch.cuda.synchronize()
+    ref = {}
+    for i, vals, idx, y in outs:
+        N, V, K, S = cases[i]
+        if i not in ref:
+            xh = to_host(xs[i])
+            ref[i] = (oracle.topk(xh, K, "f32"), oracle.softmax(xh))
+        (v64, z64), y64 = ref[i]
+        assert_topk_equal(to_host(vals), to_host(idx), v64, z64, f"two streams {cases[i]}")
+        assert_softmax_close(to_host(y), y64, f"two streams softmax {cases[i]}")
 
 
 def test_split_merge_many_partials(dev):
