@@ -1,4 +1,4 @@
-"""Independent brute-force checkers used to pin the oracle.
+"""Independent brute-force references used to pin the oracle.
 
 These share nothing with ``oracle/``: softmax is evaluated with Python's
 ``decimal`` module at 50 significant digits (Eq. 1 of Section 2, which equals
