@@ -78,6 +78,9 @@ __global__ __launch_bounds__(C::NT) void proj_logits(const uint16_t* __restrict_
             y0 = vy0;
         },
         [&](int64_t, int64_t x0, int64_t y0, f32x16 (&acc)[C::MI][C::NI]) {
+            // streaming stores: the logits are not read again by this kernel
+            // (measured 11-12% faster at 4000 x 1024 x 32000, also for a top-k
+            // reading them next; neutral at H = 4096)
 #pragma unroll
             for (int mi = 0; mi < C::MI; ++mi)
 #pragma unroll
@@ -86,7 +89,8 @@ __global__ __launch_bounds__(C::NT) void proj_logits(const uint16_t* __restrict_
                     for (int i = 0; i < 16; ++i) {
                         const int64_t row = x0 + wx * 32 * C::MI + mi * 32 + row_in_32(i, lane);
                         const int64_t col = y0 + wy * 32 * C::NI + ni * 32 + (lane & 31);
-                        if (row < N && col < V) out[row * V + col] = acc[mi][ni][i];
+                        if (row < N && col < V)
+                            __builtin_nontemporal_store(acc[mi][ni][i], out + row * V + col);
                     }
         });
 }
