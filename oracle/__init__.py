@@ -14,8 +14,10 @@ bfloat16 given as raw ``uint16`` bit patterns with ``dtype="bf16"``):
 * :func:`md_online`      -- (m, d) by the online recurrence of Alg. 3.
 * :func:`md_combine`     -- the merge operator of Eq. 4 (Section 3.1).
 * :func:`topk`           -- Eq. 5 by a full sort, ties to the lower index.
-* :func:`topk_alg4`      -- the fused single pass of Alg. 4 (Section 4).
+* :func:`topk_select`    -- Eq. 5 by K selection passes, with the online
+  normalizer of Alg. 3 (a second route to :func:`topk`, used to pin it).
 * :func:`bf16_round`     -- binary64 -> bfloat16, round to nearest even.
+* :func:`bf16_to_f64`    -- bfloat16 patterns -> binary64, exactly.
 * :func:`proj`           -- the projection ahead of the softmax (Section 1):
   logits = h . w^T in binary64.
 """
@@ -58,7 +60,7 @@ class Oracle:
         for name in ("orc_md_direct", "orc_md_online"):
             getattr(lib, name).argtypes = [vp, i32, i64, i64, vp, vp]
             getattr(lib, name).restype = i32
-        for name in ("orc_topk", "orc_topk_alg4"):
+        for name in ("orc_topk", "orc_topk_select"):
             getattr(lib, name).argtypes = [vp, i32, i64, i64, i32, vp, vp]
             getattr(lib, name).restype = i32
         lib.orc_proj.argtypes = [vp, i32, vp, i32, i64, i64, i64, vp]
@@ -67,6 +69,8 @@ class Oracle:
         lib.orc_md_combine.restype = None
         lib.orc_bf16_round.argtypes = [vp, i64, vp]
         lib.orc_bf16_round.restype = None
+        lib.orc_bf16_widen.argtypes = [vp, i64, vp]
+        lib.orc_bf16_widen.restype = None
         lib.orc_set_threads.argtypes = [i32]
         lib.orc_set_threads.restype = None
         lib.orc_get_threads.argtypes = []
@@ -129,13 +133,15 @@ class Oracle:
         _check(self.lib.orc_topk(_ptr(x), dt, n, v, int(k), _ptr(vals), _ptr(idx)), "topk")
         return vals, idx
 
-    def topk_alg4(self, x: np.ndarray, k: int, dtype: str | None = None):
-        """Alg. 4: online (m, d) plus the running sorted top-k buffer."""
+    def topk_select(self, x: np.ndarray, k: int, dtype: str | None = None):
+        """Eq. 5 by K selection passes (each the first element, under (x desc,
+        index asc), ranked after the previous pick), values from the online
+        pair of Alg. 3; returns (v, z) like :meth:`topk`."""
         x, dt, n, v = _prep(x, dtype)
         vals = np.empty((n, k), np.float64)
         idx = np.empty((n, k), np.int32)
-        _check(self.lib.orc_topk_alg4(_ptr(x), dt, n, v, int(k), _ptr(vals), _ptr(idx)),
-               "topk_alg4")
+        _check(self.lib.orc_topk_select(_ptr(x), dt, n, v, int(k), _ptr(vals), _ptr(idx)),
+               "topk_select")
         return vals, idx
 
     def proj(self, h: np.ndarray, w: np.ndarray, hdtype: str | None = None,
@@ -156,6 +162,14 @@ class Oracle:
         y = np.ascontiguousarray(y, dtype=np.float64)
         out = np.empty(y.shape, np.uint16)
         self.lib.orc_bf16_round(_ptr(y), y.size, _ptr(out))
+        return out
+
+    def bf16_to_f64(self, bits: np.ndarray) -> np.ndarray:
+        """bfloat16 bit patterns (uint16) -> binary64, exactly (the widening
+        of every bfloat16 input of the oracle)."""
+        b = np.ascontiguousarray(bits, dtype=np.uint16)
+        out = np.empty(b.shape, np.float64)
+        self.lib.orc_bf16_widen(_ptr(b), b.size, _ptr(out))
         return out
 
 
@@ -239,8 +253,8 @@ def topk(x, k, dtype=None):
     return _get().topk(x, k, dtype)
 
 
-def topk_alg4(x, k, dtype=None):
-    return _get().topk_alg4(x, k, dtype)
+def topk_select(x, k, dtype=None):
+    return _get().topk_select(x, k, dtype)
 
 
 def bf16_round(y):
@@ -251,7 +265,5 @@ def proj(h, w, hdtype=None, wdtype=None):
     return _get().proj(h, w, hdtype, wdtype)
 
 
-def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
-    """bfloat16 bit patterns (uint16) -> binary64, exactly."""
-    b = np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << 16
-    return b.view(np.float32).astype(np.float64)
+def bf16_to_f64(bits):
+    return _get().bf16_to_f64(bits)

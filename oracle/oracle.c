@@ -242,60 +242,48 @@ int orc_topk(const void* x, int dtype, int64_t N, int64_t V, int K, double* v,
     return err ? ORC_ENOMEM : ORC_OK;
 }
 
-/* Top-k by the fused single pass of Alg. 4, in its own order of steps: the
- * running pair (m, d) as in Alg. 3, plus a buffer u of K+1 values and p of
- * K+1 indices (initially -inf and -1); every element is placed in the spare
- * last slot and moved towards the front while the value ahead of it is
- * strictly smaller.  Output v_i = e^{u_i - m}/d, z_i = p_i.  This is a second,
- * independent route to the result of orc_topk, used to pin it.  Where fewer
- * than K elements beat -inf, the untouched slots keep p = -1.               */
-int orc_topk_alg4(const void* x, int dtype, int64_t N, int64_t V, int K, double* v,
-                  int32_t* z) {
-    if (bad_args(x, dtype, N, V) || K < 1 || V > INT32_MAX) return ORC_EINVAL;
+/* Top-k (Eq. 5) by repeated selection, a second route to orc_topk's result
+ * used to pin it: pass k scans the whole row for the first element, under the
+ * total order of the file header, among those ranked after the element pass
+ * k-1 took (pass 0: among all).  Its normalizer comes from the online
+ * recurrence (Alg. 3, each step an Eq. 4 merge), not from the closed form
+ * orc_topk uses.  Output v_k = e^{x_{z_k} - m}/d.                           */
+static int ranks_before(double xa, int64_t ia, double xb, int64_t ib) {
+    int an = xa != xa, bn = xb != xb;
+    if (an != bn) return bn; /* every number before every NaN */
+    if (!an && xa != xb) return xa > xb;
+    return ia < ib;          /* equal values (or two NaN): lower index first */
+}
+
+int orc_topk_select(const void* x, int dtype, int64_t N, int64_t V, int K, double* v,
+                    int32_t* z) {
+    if (bad_args(x, dtype, N, V) || K < 1 || K > V || V > INT32_MAX) return ORC_EINVAL;
     if (N > 0 && (!v || !z)) return ORC_EINVAL;
-    int err = 0;
-#pragma omp parallel num_threads(orc_get_threads())
-    {
-        double* u = (double*)malloc((size_t)(K + 1) * sizeof(double));
-        int32_t* p = (int32_t*)malloc((size_t)(K + 1) * sizeof(int32_t));
-        if (!u || !p) {
-#pragma omp atomic write
-            err = 1;
-        }
-#pragma omp for schedule(dynamic, 1)
-        for (int64_t r = 0; r < N; ++r) {
-            if (!u || !p) continue;
-            const void* row = row_ptr(x, dtype, V, r);
-            double m = -INFINITY, d = 0.0;
-            for (int k = 0; k <= K; ++k) {
-                u[k] = -INFINITY;
-                p[k] = -1;
-            }
+#pragma omp parallel for schedule(dynamic, 1) num_threads(orc_get_threads())
+    for (int64_t r = 0; r < N; ++r) {
+        const void* row = row_ptr(x, dtype, V, r);
+        double m, d;
+        md_online_row(row, dtype, V, &m, &d);
+        double prev_x = 0.0;
+        int64_t prev_i = -1;
+        for (int k = 0; k < K; ++k) {
+            int64_t best = -1;
+            double best_x = 0.0;
             for (int64_t j = 0; j < V; ++j) {
                 double xj = load_elem(row, dtype, j);
-                orc_md_combine(m, d, xj, 1.0, &m, &d);
-                u[K] = xj;
-                p[K] = (int32_t)j;
-                int k = K - 1;
-                while (k >= 0 && u[k] < u[k + 1]) {
-                    double tu = u[k];
-                    u[k] = u[k + 1];
-                    u[k + 1] = tu;
-                    int32_t tp = p[k];
-                    p[k] = p[k + 1];
-                    p[k + 1] = tp;
-                    --k;
+                if (prev_i >= 0 && !ranks_before(prev_x, prev_i, xj, j)) continue;
+                if (best < 0 || ranks_before(xj, j, best_x, best)) {
+                    best = j;
+                    best_x = xj;
                 }
             }
-            for (int k = 0; k < K; ++k) {
-                v[r * K + k] = exp(u[k] - m) / d;
-                z[r * K + k] = p[k];
-            }
+            z[r * K + k] = (int32_t)best;
+            v[r * K + k] = exp(best_x - m) / d;
+            prev_x = best_x;
+            prev_i = best;
         }
-        free(u);
-        free(p);
     }
-    return err ? ORC_ENOMEM : ORC_OK;
+    return ORC_OK;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -323,6 +311,12 @@ static uint16_t bf16_from_f64(double a) {
 
 void orc_bf16_round(const double* y, int64_t n, uint16_t* out) {
     for (int64_t i = 0; i < n; ++i) out[i] = bf16_from_f64(y[i]);
+}
+
+/* bfloat16 bit patterns to binary64, exactly: the widening every bfloat16
+ * input of the oracle goes through (load_elem). */
+void orc_bf16_widen(const uint16_t* bits, int64_t n, double* out) {
+    for (int64_t i = 0; i < n; ++i) out[i] = load_elem(bits, ORC_BF16, i);
 }
 
 /* ------------------------------------------------------------ projection */

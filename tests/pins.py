@@ -217,14 +217,15 @@ def check_topk_library(orc):
             np.testing.assert_array_equal(vals[r], y[r, idx[r]])
 
 
-def check_topk_alg4(orc):
-    """Alg. 4's fused single pass agrees with the sort, ties included."""
+def check_topk_select(orc):
+    """K selection passes (Eq. 5 taken one rank at a time, online normalizer)
+    agree with the sort, ties included."""
     rng = _rng(10)
     for trial in range(30):
         V = int(rng.integers(1, 400))
         K = int(rng.integers(1, min(V, 20) + 1))
         x = np.round(rng.standard_normal((2, V)) * 2, 1).astype(np.float32)
-        v4, z4 = orc.topk_alg4(x, K)
+        v4, z4 = orc.topk_select(x, K)
         vs, zs = orc.topk(x, K)
         assert np.array_equal(z4, zs), (V, K)
         np.testing.assert_allclose(v4, vs, rtol=1e-13, atol=0)
@@ -240,6 +241,24 @@ def check_topk_signed_zero(orc):
 # --------------------------------------------------------------- bfloat16 ---
 def _bf16_to_f64(bits):
     return (np.asarray(bits, np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def check_bf16_widening(orc):
+    """Every one of the 65536 bfloat16 patterns widens to the value torch's
+    bfloat16 -> float32 conversion gives (exact by the format's definition:
+    the pattern is the upper half of a binary32), signed zeros and
+    infinities included; NaN patterns stay NaN."""
+    allb = np.arange(0, 1 << 16, dtype=np.uint32).astype(np.uint16)
+    got = orc.bf16_to_f64(allb)
+    ref = torch.from_numpy(allb.view(np.int16)).view(torch.bfloat16).float().numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    ref64 = ref[~nan].astype(np.float64)  # signalling NaN patterns left out of the cast
+    assert np.array_equal(got[~nan], ref64)
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref64))
+    # a few patterns by hand: 1.0, -2.0, the smallest subnormal, -inf
+    assert orc.bf16_to_f64(np.array([0x3F80, 0xC000, 0x0001, 0xFF80], np.uint16)).tolist() == \
+        [1.0, -2.0, 2.0 ** -133, -math.inf]
 
 
 def check_bf16_rounding(orc):
@@ -327,6 +346,7 @@ ALL = [
     check_softmax_closed_forms, check_softmax_shift_and_overflow,
     check_softmax_nonfinite, check_theorem1, check_prefix_bound,
     check_combine_algebra, check_topk_enumeration, check_topk_library,
-    check_topk_alg4, check_topk_signed_zero, check_bf16_rounding, check_golden,
+    check_topk_select, check_topk_signed_zero, check_bf16_widening, check_bf16_rounding,
+    check_golden,
     check_projection,
 ]

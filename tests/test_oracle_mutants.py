@@ -52,9 +52,15 @@ MUTANTS = {
     "topk_value_off_by_one": (
         "z[r * K + k] = buf[k].i;\n                v[r * K + k] = exp(buf[k].x - m) / d;",
         "z[r * K + k] = buf[k].i;\n                v[r * K + k] = exp(buf[k + (k + 1 < K)].x - m) / d;"),
-    "alg4_non_strict_insertion": (
-        "while (k >= 0 && u[k] < u[k + 1]) {",
-        "while (k >= 0 && u[k] <= u[k + 1]) {"),
+    "select_ties_to_higher_index": (
+        "return ia < ib;          /* equal values",
+        "return ia > ib;          /* equal values"),
+    "select_skips_last_element": (
+        "for (int64_t j = 0; j < V; ++j) {\n                double xj = load_elem(row, dtype, j);\n                if (prev_i",
+        "for (int64_t j = 0; j + 1 < V; ++j) {\n                double xj = load_elem(row, dtype, j);\n                if (prev_i"),
+    "bf16_widen_reads_wrong_type": (
+        "out[i] = load_elem(bits, ORC_BF16, i);",
+        "out[i] = load_elem(bits, ORC_F32, i / 2);"),
     "bf16_round_half_away": (
         "double r = rint(a / q) * q;",
         "double r = round(a / q) * q;"),
@@ -98,3 +104,15 @@ def test_mutant_is_caught(name, tmp_path):
     lib = oracle.build(str(src), str(tmp_path / "liboracle_mutant.so"))
     caught = _first_failure(oracle.load(lib))
     assert caught is not None, f"no pin caught mutant {name}"
+
+
+def test_widening_pin_catches_wrong_shift(tmp_path):
+    """The bfloat16 widening pin on its own catches a widening off by one bit
+    position (the expected values of every bfloat16 GPU check go through it)."""
+    old, new = MUTANTS["bf16_widening_wrong_shift"]
+    text = open(SRC).read()
+    src = tmp_path / "oracle.c"
+    src.write_text(text.replace(old, new))
+    lib = oracle.build(str(src), str(tmp_path / "liboracle_mutant.so"))
+    with pytest.raises(AssertionError):
+        pins.check_bf16_widening(oracle.load(lib))
