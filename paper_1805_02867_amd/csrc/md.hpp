@@ -32,6 +32,43 @@ constexpr float kEmptyS = -3.402823466e38f;  // -FLT_MAX: identity of the merge
 
 __device__ __forceinline__ float exp2_hw(float v) { return __builtin_amdgcn_exp2f(v); }
 
+// Outputs y = 2^t * rd (t = x log2e - s, rd = 1/d).  v_exp_f32 returns 0
+// where 2^t is below 2^-126 (it produces no binary32 subnormals), which would
+// lose outputs that are subnormal but not zero.  There the exponent is raised
+// by 64 and the factor 2^-64 moved into rd: 2^{t+64} is normal for every
+// t >= -190 and the product rounds once, to the subnormal result.  (rd *
+// 2^-64 stays normal for d <= 2^62, which holds for the safe and online
+// normalizers: d <= V * 2^8.)
+constexpr float kExpMin = -126.0f;
+
+__device__ __forceinline__ float out_scaled(float t, float rd) {
+    const bool lo = t < kExpMin;
+    return exp2_hw(lo ? t + 64.0f : t) * (lo ? rd * 0x1p-64f : rd);
+}
+
+__device__ __forceinline__ float out_elem(float x, float S, float rd) {
+    return out_scaled(__builtin_fmaf(x, kLog2e, -S), rd);
+}
+
+// The same for N values at once: the common case (no exponent below -126 in
+// the wavefront) costs one minimum per element pair and one uniform branch.
+template <int N>
+__device__ __forceinline__ void out_vals(float (&v)[N], float S, float rd) {
+    float t[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) t[i] = __builtin_fmaf(v[i], kLog2e, -S);
+    float mn = t[0];
+#pragma unroll
+    for (int i = 1; i < N; ++i) mn = __builtin_fminf(mn, t[i]);
+    if (__builtin_amdgcn_ballot_w64(mn < kExpMin) == 0) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) v[i] = exp2_hw(t[i]) * rd;
+    } else {
+#pragma unroll
+        for (int i = 0; i < N; ++i) v[i] = out_scaled(t[i], rd);
+    }
+}
+
 // ---------------------------------------------------------------- element I/O
 // Native 16-byte vector types (the nontemporal builtins take these).
 typedef float f32x4 __attribute__((ext_vector_type(4)));

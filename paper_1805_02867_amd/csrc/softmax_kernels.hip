@@ -171,8 +171,9 @@ __device__ __forceinline__ float lane_sum(const Range<T>& r, int t, float S) {
     return acc;
 }
 
-// Output pass: y = 2^{x log2e - S} * (1/d), stored with non-temporal hints so
-// that the written rows do not evict input rows still waiting for this pass.
+// Output pass: y = 2^{x log2e - S} * (1/d) (subnormal results included, see
+// out_vals), stored with non-temporal hints so that the written rows do not
+// evict input rows still waiting for this pass.
 template <typename T, int TEAM, int U, bool NT = OSM_NT_LAST>
 __device__ __forceinline__ void lane_out(const Range<T>& r, int t, float S, float rd) {
     constexpr int E = Vec<T>::N;
@@ -185,22 +186,18 @@ __device__ __forceinline__ void lane_out(const Range<T>& r, int t, float S, floa
         for (int u = 0; u < U; ++u) buf[u] = vload<T, NT>(vb + (v + (int64_t)u * TEAM) * E);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-#pragma unroll
-            for (int i = 0; i < E; ++i)
-                buf[u].v[i] = exp2_hw(__builtin_fmaf(buf[u].v[i], kLog2e, -S)) * rd;
+            out_vals(buf[u].v, S, rd);
             buf[u].store_nt(yb + (v + (int64_t)u * TEAM) * E);
         }
     }
     for (; v < r.nvec; v += TEAM) {
         Vec<T> b = vload<T, NT>(vb + v * E);
-#pragma unroll
-        for (int i = 0; i < E; ++i) b.v[i] = exp2_hw(__builtin_fmaf(b.v[i], kLog2e, -S)) * rd;
+        out_vals(b.v, S, rd);
         b.store_nt(yb + v * E);
     }
-    for (int64_t i = t; i < r.head; i += TEAM)
-        store1(r.yb + i, exp2_hw(__builtin_fmaf(load1(r.xb + i), kLog2e, -S)) * rd);
+    for (int64_t i = t; i < r.head; i += TEAM) store1(r.yb + i, out_elem(load1(r.xb + i), S, rd));
     for (int64_t i = r.tail0 + t; i < r.n; i += TEAM)
-        store1(r.yb + i, exp2_hw(__builtin_fmaf(load1(r.xb + i), kLog2e, -S)) * rd);
+        store1(r.yb + i, out_elem(load1(r.xb + i), S, rd));
 }
 
 // --------------------------------------------------------------- row kernels

@@ -110,8 +110,7 @@ __global__ __launch_bounds__(BLOCK) void softmax_resident(const T* __restrict__ 
             if (ok[i]) {
                 Vec<T> o;
                 widen_vec<T>(buf[i], o.v);
-#pragma unroll
-                for (int k = 0; k < E; ++k) o.v[k] = exp2_hw(__builtin_fmaf(o.v[k], kLog2e, -S)) * rd;
+                out_vals(o.v, S, rd);
                 T* dst = yv + (t + (int64_t)i * BLOCK) * E;
                 if constexpr (YVEC) {
                     o.store_nt(dst);
@@ -121,8 +120,8 @@ __global__ __launch_bounds__(BLOCK) void softmax_resident(const T* __restrict__ 
                 }
             }
         }
-        if (hok) store1(yr + t, exp2_hw(__builtin_fmaf(hx, kLog2e, -S)) * rd);
-        if (tok) store1(yr + tail0 + t, exp2_hw(__builtin_fmaf(tx, kLog2e, -S)) * rd);
+        if (hok) store1(yr + t, out_elem(hx, S, rd));
+        if (tok) store1(yr + tail0 + t, out_elem(tx, S, rd));
     }
 }
 

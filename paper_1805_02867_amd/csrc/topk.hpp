@@ -783,7 +783,7 @@ __device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restric
             vals[row * K + lane] = key_value(key);
         } else {
             const float S = md.s, rd = 1.0f / md.d;
-            vals[row * K + lane] = exp2_hw(__builtin_fmaf(key_value(key), kLog2e, -S)) * rd;
+            vals[row * K + lane] = out_elem(key_value(key), S, rd);
         }
         idx[row * K + lane] = key_index(key);
     }
@@ -865,7 +865,7 @@ __device__ __forceinline__ void topk_merge_row(uint64_t* region, const uint64_t*
             vals[row * K + lane] = key_value(key);
         } else {
             const float Sv = md.s, rd = 1.0f / md.d;
-            vals[row * K + lane] = exp2_hw(__builtin_fmaf(key_value(key), kLog2e, -Sv)) * rd;
+            vals[row * K + lane] = out_elem(key_value(key), Sv, rd);
         }
         idx[row * K + lane] = key_index(key);
     }

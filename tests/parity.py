@@ -1,14 +1,14 @@
 """Comparison rules between the HIP path and the binary64 oracle.
 
 binary32 outputs: |y - y64| <= 1e-5 * y64 elementwise; where y64 is below the
-smallest normal binary32 (2^-126), |y - y64| <= 2^-126 instead (such values
-are subnormal or flushed in any binary32 implementation).  NaN where the
-oracle gives NaN.
+smallest normal binary32 (2^-126), |y - y64| <= 2^-126 instead (a subnormal
+binary32 holds fewer than 24 significant bits, so a relative bound cannot
+hold there; tests of the subnormal range check these outputs more tightly
+themselves).  NaN where the oracle gives NaN.
 
 bfloat16 outputs: the bit pattern is within 1 unit in the last place of the
-oracle's value rounded to bfloat16 (to nearest even, from binary64); where
-y64 is below 2^-126 the binary32 floor above applies instead (the hardware
-exponential flushes subnormal results, so such outputs may read 0).
+oracle's value rounded to bfloat16 (to nearest even, from binary64),
+subnormal values included.
 
 top-k: indices bit-exact; values by the binary32 rule against y64 at the
 oracle's indices.
@@ -57,9 +57,7 @@ def assert_softmax_close(y: np.ndarray, y64: np.ndarray, what: str = ""):
         gw = want.astype(np.int32)
         is_nan_gpu = ((gy & 0x7F80) == 0x7F80) & ((gy & 0x007F) != 0)
         ulp = np.abs(gy - gw)
-        yval = (gy.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-        tiny_ok = (y64 < FLT_MIN) & (np.abs(yval - y64) <= FLT_MIN)
-        bad = np.where(nan64, ~is_nan_gpu, (ulp > 1) & ~tiny_ok)
+        bad = np.where(nan64, ~is_nan_gpu, ulp > 1)
         if bad.any():
             r, c = np.argwhere(bad)[0]
             raise AssertionError(

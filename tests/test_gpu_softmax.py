@@ -194,3 +194,44 @@ def test_ref_stream_copy_is_exact(dev):
     osm.ref_stream("read", x, sink)
     torch.cuda.synchronize()
     assert torch.equal(x, y)
+
+
+def _subnormal_rows(V: int, tdt):
+    """Rows whose outputs sweep through the binary32 and bfloat16 subnormal
+    range: the row maximum is 0 and the rest descend from -80 to -110 (e^-87.3
+    is 2^-126, e^-92.2 the smallest bfloat16 subnormal 2^-133, e^-103.3 the
+    smallest binary32 subnormal 2^-149)."""
+    base = np.linspace(-80.0, -110.0, V - 1)
+    rows = [np.concatenate([[0.0], base]), np.concatenate([base[::-1], [0.0]]),
+            np.concatenate([base[: V // 2], [0.0], base[V // 2:]])]
+    return torch.tensor(np.array(rows), dtype=tdt)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_subnormal_outputs(dev, dtype):
+    """Outputs below 2^-126 are rounded, not flushed: bfloat16 within 1 ulp of
+    the oracle's rounding (no exception for subnormals), binary32 within the
+    normal range's relative bound plus one subnormal unit, 1e-5 y64 + 2^-149,
+    where the oracle is subnormal."""
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    for V in (301, 4001):
+        x = _subnormal_rows(V, tdt).to(dev)
+        xh = to_host(x)
+        y64 = oracle.softmax(xh, host_dtype(x))
+        assert (y64 < 2.0 ** -126).sum() > 30 and (y64 > 2.0 ** -149).sum() > 30
+        cases = [(m, osm.KERNEL_ROWS, t) for m in MODES for t in (8, 64, 256, 1024)]
+        cases += [(m, osm.KERNEL_SPLIT, s) for m in MODES for s in (1, 3)]
+        cases += [("resident", osm.KERNEL_AUTO, 0)]
+        for mode, kernel, param in cases:
+            what = f"subnormal {dtype} V={V} {mode} kernel {kernel} param {param}"
+            print(what, flush=True)
+            y = osm.softmax_fwd(x, mode=mode, kernel=kernel, param=param)
+            torch.cuda.synchronize()
+            yh = to_host(y)
+            assert_softmax_close(yh, y64, what)
+            if dtype == "f32":
+                tiny = y64 < 2.0 ** -126
+                err = np.abs(yh.astype(np.float64) - y64)[tiny]
+                bound = 1e-5 * y64[tiny] + 2.0 ** -149
+                assert (err <= bound).all(), (what, (err / bound).max())
+                assert (yh[tiny] > 0).sum() >= (y64[tiny] >= 2.0 ** -148).sum()

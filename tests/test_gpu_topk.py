@@ -240,3 +240,34 @@ def test_split_merge_many_partials(dev):
         torch.cuda.synchronize()
         v64, z64 = oracle.topk(to_host(t), K, "f32")
         assert_topk_equal(to_host(vals), to_host(idx), v64, z64, f"split merge ties {N}x{V} K={K} S={S}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_subnormal_values(dev, dtype):
+    """Top-k values below 2^-126 are rounded, not flushed: the row maximum is 0
+    and the next largest elements sit at -88 ... -100, so the K-th value is a
+    binary32 subnormal; each value within 1e-5 of the oracle's plus one
+    subnormal unit (2^-149)."""
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    V = 5000
+    rows = []
+    for r in range(6):
+        row = np.full(V, -200.0)
+        row[(r * 997) % V] = 0.0
+        pos = (np.arange(12) * 389 + r * 17) % V
+        pos = pos[pos != (r * 997) % V]
+        row[pos] = -88.0 - np.arange(len(pos))
+        rows.append(row)
+    x = torch.tensor(np.array(rows), dtype=tdt, device=dev)
+    K = 10
+    cases = [(osm.KERNEL_ROWS, p) for p in SHAPES] + [(osm.KERNEL_SPLIT, 3)]
+    for kernel, param in cases:
+        vals, idx = osm.softmax_topk(x, K, kernel=kernel, param=param)
+        torch.cuda.synchronize()
+        v64, z64 = oracle.topk(to_host(x), K, host_dtype(x))
+        what = f"subnormal top-k {dtype} kernel {kernel} param {param}"
+        assert_topk_equal(to_host(vals), to_host(idx), v64, z64, what)
+        assert (v64 < 2.0 ** -126).sum() > 20
+        err = np.abs(to_host(vals).astype(np.float64) - v64)
+        tiny = v64 < 2.0 ** -126
+        assert (err[tiny] <= 1e-5 * v64[tiny] + 2.0 ** -149).all(), what
