@@ -28,12 +28,17 @@
  *    below 2.35e38 (x * log2(e) must be finite).  Top-k of a NaN row is
  *    unspecified.
  *  - Thread safety: calls may be made concurrently from several host threads
- *    and streams.  The shared state is a per-device cache of device
- *    properties, a per-device stream-ordered memory pool, and the scratch of
- *    the split kernels, kept per stream (up to 64 streams per device; a
- *    buffer grows in stream order and is kept until the process ends; work
- *    of a destroyed stream must have finished before a new stream with the
- *    same handle calls the library).
+ *    and streams, including several threads on one stream.  The shared state
+ *    is a per-device cache of device properties, a per-device stream-ordered
+ *    memory pool, and the scratch of the split kernels, kept per stream (up
+ *    to 64 streams per device; further streams get a buffer per call).  A
+ *    call that uses its stream's scratch holds a per-device lock from taking
+ *    the buffer until its last kernel is enqueued, so calls on one stream
+ *    never interleave their kernels on shared buffers.  A stream's buffer
+ *    grows in stream order and is kept until osm_stream_release(stream) or
+ *    the end of the process: call osm_stream_release before destroying a
+ *    stream that has used the library, so that a later stream given the same
+ *    handle starts without a buffer.
  */
 #ifndef OSOFTMAX_H
 #define OSOFTMAX_H
@@ -239,6 +244,15 @@ OSM_API int proj_softmax_topk(const void* h, const void* w, float* vals, int32_t
  * Errors: OSM_EINVAL for another op, bytes < 0 or not
  * a multiple of 16, null or misaligned pointers, overlap. */
 OSM_API int osm_ref_stream(int op, const void* x, void* y, int64_t bytes, hipStream_t stream);
+
+/* Releases the scratch buffers the library keeps for `stream` (split
+ * kernels' partials and row counters): they are freed in stream order, behind
+ * the work already enqueued on the stream, which still completes normally;
+ * the next call on the stream allocates afresh.  Call it before destroying a
+ * stream that has used the library.  A stream without buffers is a no-op.
+ * Errors: OSM_EHIP if HIP rejects the stream-ordered free (for example a
+ * stream already destroyed). */
+OSM_API int osm_stream_release(hipStream_t stream);
 
 /* Kernel family and parameter softmax_fwd would use for this shape on the
  * current device (for OSM_RESIDENT: OSM_KERNEL_ROWS and the threads per row).  Errors: OSM_EINVAL for bad sizes, dtype or

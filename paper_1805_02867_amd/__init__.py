@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
     L.proj_softmax_topk.restype = i32
     L.osm_plan.argtypes = [i64, i64, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i64)]
     L.osm_plan.restype = i32
+    L.osm_stream_release.argtypes = [vp]
+    L.osm_stream_release.restype = i32
     L.osm_ref_stream.argtypes = [i32, vp, vp, i64, vp]
     L.osm_ref_stream.restype = i32
     L.osm_status_string.argtypes = [i32]
@@ -206,6 +208,14 @@ def topk(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,
     if rc != OK:
         raise OsmError(rc, "topk_fwd")
     return vals, idx
+
+
+def stream_release(stream=None) -> None:
+    """Frees the scratch the library keeps for `stream` (``osm_stream_release``),
+    in stream order; call before destroying a stream that used the library."""
+    rc = lib().osm_stream_release(_stream(stream))
+    if rc != OK:
+        raise OsmError(rc, "osm_stream_release")
 
 
 def topk_plan(N: int, V: int, K: int, dtype=torch.float32):

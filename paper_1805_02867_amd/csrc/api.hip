@@ -70,21 +70,35 @@ DeviceState* device_state(int* dev_out) {
     return &s;
 }
 
+// The scratch and counter tables are guarded by the device's mutex, and a
+// call that uses a stream's buffers holds it from acquiring them until its
+// last launch has been enqueued (`lk`, locked by the first acquire): calls
+// from several host threads on one stream then enqueue their kernels whole,
+// one call after another, so no call's launches land between another's on
+// the same buffers, and a buffer is replaced (its old copy freed in stream
+// order) only between calls.
+
+// Slot of `stream` in `tab`, creating it if the table has room; null if full.
+ScratchSlot* find_slot(ScratchSlot* tab, int* n, hipStream_t stream) {
+    for (int i = 0; i < *n; ++i)
+        if (tab[i].stream == stream) return &tab[i];
+    if (*n >= kScratchSlots) return nullptr;
+    ScratchSlot* slot = &tab[(*n)++];
+    *slot = ScratchSlot{stream, nullptr, 0};
+    return slot;
+}
+
 // Scratch of at least `bytes` for work enqueued on `stream`.  A stream's
 // buffer grows by a stream-ordered allocation from the library pool (the old
 // one is freed in stream order behind the work already enqueued) and is kept
-// until the process ends.  Once the table is full, a call gets a buffer of
-// its own (*temp = true) that it frees in stream order after its launches.
-int acquire_scratch(DeviceState* ds, hipStream_t stream, size_t bytes, void** out, bool* temp) {
+// until osm_stream_release or the end of the process.  Once the table is
+// full, a call gets a buffer of its own (*temp = true) that it frees in
+// stream order after its launches.
+int acquire_scratch(DeviceState* ds, std::unique_lock<std::mutex>& lk, hipStream_t stream,
+                    size_t bytes, void** out, bool* temp) {
     if (!ds->pool_ok) return OSM_ENOMEM;
-    std::lock_guard<std::mutex> guard(ds->mu);
-    ScratchSlot* slot = nullptr;
-    for (int i = 0; i < ds->nslots; ++i)
-        if (ds->slots[i].stream == stream) slot = &ds->slots[i];
-    if (!slot && ds->nslots < kScratchSlots) {
-        slot = &ds->slots[ds->nslots++];
-        *slot = ScratchSlot{stream, nullptr, 0};
-    }
+    if (!lk.owns_lock()) lk.lock();
+    ScratchSlot* slot = find_slot(ds->slots, &ds->nslots, stream);
     *temp = slot == nullptr;
     if (slot && slot->bytes >= bytes) {
         *out = slot->ptr;
@@ -113,18 +127,12 @@ int acquire_scratch(DeviceState* ds, hipStream_t stream, size_t bytes, void** ou
 // `stream`; the kernels that use it leave it zeroed.  A stream's array grows
 // by a stream-ordered allocation, cleared in stream order; once the table is
 // full, a call gets an array of its own (*temp = true) to free after its
-// launches.
-int acquire_counters(DeviceState* ds, hipStream_t stream, size_t count, uint32_t** out,
-                     bool* temp) {
+// launches.  Locking as acquire_scratch.
+int acquire_counters(DeviceState* ds, std::unique_lock<std::mutex>& lk, hipStream_t stream,
+                     size_t count, uint32_t** out, bool* temp) {
     if (!ds->pool_ok) return OSM_ENOMEM;
-    std::lock_guard<std::mutex> guard(ds->mu);
-    ScratchSlot* slot = nullptr;
-    for (int i = 0; i < ds->ncslots; ++i)
-        if (ds->cslots[i].stream == stream) slot = &ds->cslots[i];
-    if (!slot && ds->ncslots < kScratchSlots) {
-        slot = &ds->cslots[ds->ncslots++];
-        *slot = ScratchSlot{stream, nullptr, 0};
-    }
+    if (!lk.owns_lock()) lk.lock();
+    ScratchSlot* slot = find_slot(ds->cslots, &ds->ncslots, stream);
     *temp = slot == nullptr;
     const size_t bytes = count * 4;
     if (slot && slot->bytes >= bytes) {
@@ -150,6 +158,19 @@ int acquire_counters(DeviceState* ds, hipStream_t stream, size_t count, uint32_t
     }
     *out = static_cast<uint32_t*>(p);
     return OSM_OK;
+}
+
+// Drops `stream`'s slot from `tab` (its buffer freed in stream order).
+hipError_t release_slot(ScratchSlot* tab, int* n, hipStream_t stream) {
+    hipError_t e = hipSuccess;
+    for (int i = 0; i < *n; ++i) {
+        if (tab[i].stream != stream) continue;
+        if (tab[i].ptr) e = hipFreeAsync(tab[i].ptr, stream);
+        tab[i] = tab[*n - 1];
+        --*n;
+        break;
+    }
+    return e;
 }
 
 // ------------------------------------------------------------- validation
@@ -273,7 +294,8 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
     if (N * S > kMaxDim) return OSM_EINVAL;
     void* scratch = nullptr;
     bool temp = false;
-    const int st = acquire_scratch(ds, stream, (size_t)N * (size_t)S * 8, &scratch, &temp);
+    std::unique_lock<std::mutex> lk(ds->mu, std::defer_lock);  // held until the launches are in
+    const int st = acquire_scratch(ds, lk, stream, (size_t)N * (size_t)S * 8, &scratch, &temp);
     if (st != OSM_OK) return st;
     hipError_t e = osm::launch_softmax_split(x, y, scratch, N, V, dtype, mode, S, chunk, vec,
                                              stream);
@@ -324,14 +346,15 @@ int launch_topk_pass(const void* x, float* vals, int32_t* idx, int64_t N, int64_
     }
     void* scratch = nullptr;
     bool temp = false;
-    int st = acquire_scratch(ds, stream, osm::topk_part_bytes(N, S, K), &scratch, &temp);
+    std::unique_lock<std::mutex> lk(ds->mu, std::defer_lock);  // held until the launch is in
+    int st = acquire_scratch(ds, lk, stream, osm::topk_part_bytes(N, S, K), &scratch, &temp);
     if (st != OSM_OK) return st;
     a.part = scratch;
     a.S = S;
     a.chunk = chunk;
     // per-row chunk counters: each row's last chunk merges it in the same kernel
     bool ctemp = false;
-    st = acquire_counters(ds, stream, (size_t)N, &a.ctr, &ctemp);
+    st = acquire_counters(ds, lk, stream, (size_t)N, &a.ctr, &ctemp);
     if (st != OSM_OK) {
         if (temp) (void)hipFreeAsync(scratch, stream);
         return st;
@@ -448,7 +471,9 @@ int run_proj_topk(const void* h, const void* w, float* vals, int32_t* idx, int64
     osm::proj_topk_shape(N, V, K, ds->cus, &S, &tiles, &parts);
     void* scratch = nullptr;
     bool temp = false;
-    st = acquire_scratch(ds, stream, osm::proj_topk_part_bytes(N, S, parts, K), &scratch, &temp);
+    std::unique_lock<std::mutex> lk(ds->mu, std::defer_lock);  // held until the launches are in
+    st = acquire_scratch(ds, lk, stream, osm::proj_topk_part_bytes(N, S, parts, K), &scratch,
+                         &temp);
     if (st != OSM_OK) return st;
     hipError_t e =
         osm::launch_proj_topk(h, w, vals, idx, scratch, N, H, V, K, S, tiles, parts, stream);
@@ -530,6 +555,19 @@ int proj_fwd(const void* h, const void* w, float* logits, int64_t N, int64_t H, 
 int proj_softmax_topk(const void* h, const void* w, float* vals, int32_t* idx, int64_t N,
                       int64_t H, int64_t V, int K, hipStream_t stream) {
     return run_proj_topk(h, w, vals, idx, N, H, V, K, stream);
+}
+
+int osm_stream_release(hipStream_t stream) {
+    DeviceState* ds = device_state(nullptr);
+    if (!ds) return OSM_EHIP;
+    std::lock_guard<std::mutex> guard(ds->mu);
+    const hipError_t e = release_slot(ds->slots, &ds->nslots, stream);
+    const hipError_t f = release_slot(ds->cslots, &ds->ncslots, stream);
+    if (e != hipSuccess || f != hipSuccess) {
+        (void)hipGetLastError();
+        return OSM_EHIP;
+    }
+    return OSM_OK;
 }
 
 int osm_plan(int64_t N, int64_t V, int dtype, int mode, int* kernel, int64_t* param) {

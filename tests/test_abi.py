@@ -24,7 +24,7 @@ def test_header_declares_the_boundary():
     for want in ("softmax_fwd", "softmax_fwd_ex", "softmax_topk", "softmax_topk_dt",
                  "softmax_topk_ex", "softmax_topk_algo", "topk_fwd", "proj_fwd",
                  "proj_softmax_topk", "osm_plan", "osm_topk_plan", "osm_status_string",
-                 "osm_ref_stream"):
+                 "osm_ref_stream", "osm_stream_release"):
         assert want in names
 
 
