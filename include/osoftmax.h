@@ -85,7 +85,9 @@ enum osm_status {
     OSM_EINVAL = 1,       /* invalid argument; nothing enqueued */
     OSM_EUNSUPPORTED = 2, /* valid but unsupported configuration */
     OSM_EHIP = 3,         /* HIP reported an error while enqueuing */
-    OSM_ENOMEM = 4        /* scratch allocation failed */
+    OSM_ENOMEM = 4,       /* scratch allocation failed */
+    OSM_ESCRATCH = 5      /* needs more than OSM_NOALLOC_SCRATCH_BYTES of
+                             fixed scratch (softmax_topk_ex_noalloc) */
 };
 
 /* Kernel families for softmax_fwd_ex, softmax_topk_ex and softmax_topk_algo. */
@@ -180,6 +182,29 @@ OSM_API int softmax_topk_dt(const void* x, float* vals, int32_t* idx, int64_t N,
  * bytes) or the row counters (4N bytes) cannot be allocated. */
 OSM_API int softmax_topk_ex(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V,
                             int K, int dtype, int kernel, int64_t param, hipStream_t stream);
+
+/* Size of the fixed scratch array behind softmax_topk_ex_noalloc, per device. */
+#define OSM_NOALLOC_SCRATCH_BYTES (1u << 20)
+
+/* softmax_topk_ex for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops that must not call hipMalloc): the same
+ * kernels and results, but nothing is allocated or freed, by the library or
+ * through any allocating routine.  The split path (OSM_KERNEL_SPLIT, or the
+ * plan's choice for small batches of long rows) keeps its per-chunk partials
+ * (N * S * (8K + 8) bytes, rounded up to 256) and its N row counters (4N
+ * bytes, cleared by a small kernel at each call) in a fixed array of
+ * OSM_NOALLOC_SCRATCH_BYTES per device, held until the process ends; the row
+ * kernels need no scratch.  Every call on a device shares that array, and it
+ * keeps the last call's contents: calls that can overlap on one device (on
+ * different streams, or from host threads on different streams) race and
+ * must be ordered by the caller; calls on one stream are ordered by the
+ * stream.  Arguments, results and errors as softmax_topk_ex, plus
+ * OSM_ESCRATCH when the split path would need more than the array holds
+ * (nothing enqueued) and OSM_EHIP if the array's device address could not
+ * be obtained. */
+OSM_API int softmax_topk_ex_noalloc(const void* x, float* vals, int32_t* idx, int64_t N,
+                                    int64_t V, int K, int dtype, int kernel, int64_t param,
+                                    hipStream_t stream);
 
 /* Softmax + top-k by any osm_topk_algo, with an explicit kernel for the
  * top-k pass (kernel and param as in softmax_topk_ex; the two-wavefront

@@ -18,7 +18,8 @@ F32, BF16 = 0, 1
 NAIVE, SAFE, ONLINE, RESIDENT = 0, 1, 2, 3
 RESIDENT_MAX_VEC = 16384
 KERNEL_AUTO, KERNEL_ROWS, KERNEL_SPLIT = 0, 1, 2
-OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM = 0, 1, 2, 3, 4
+OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM, ESCRATCH = 0, 1, 2, 3, 4, 5
+NOALLOC_SCRATCH_BYTES = 1 << 20
 TOPK_KMAX = 64
 PROJ_KMAX = 16
 TOPK_ONLINE_FUSED, TOPK_SAFE_FUSED, TOPK_SAFE_UNFUSED, TOPK_ONLINE_UNFUSED, TOPK_VALUES = range(5)
@@ -59,6 +60,8 @@ def lib() -> ctypes.CDLL:
     L.softmax_topk_dt.restype = i32
     L.softmax_topk_ex.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, i64, vp]
     L.softmax_topk_ex.restype = i32
+    L.softmax_topk_ex_noalloc.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, i64, vp]
+    L.softmax_topk_ex_noalloc.restype = i32
     L.softmax_topk_algo.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, i32, i64, vp]
     L.softmax_topk_algo.restype = i32
     L.topk_fwd.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
@@ -195,6 +198,22 @@ def softmax_topk(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,
 
 
 softmax_topk_dt = softmax_topk
+
+
+def softmax_topk_noalloc(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,
+                         idx: torch.Tensor | None = None, stream=None,
+                         kernel: int = KERNEL_AUTO, param: int = 0):
+    """(vals, idx) as softmax_topk, through ``softmax_topk_ex_noalloc``: the
+    library allocates nothing (split partials in its fixed per-device scratch
+    array).  Calls that can overlap on one device race on that array."""
+    N, V = _batch(x)
+    vals, idx = _topk_outputs(x, N, K, vals, idx)
+    rc = lib().softmax_topk_ex_noalloc(x.data_ptr(), vals.data_ptr(), idx.data_ptr(), N, V,
+                                       int(K), _DTYPES[x.dtype], int(kernel), int(param),
+                                       _stream(stream))
+    if rc != OK:
+        raise OsmError(rc, "softmax_topk_ex_noalloc")
+    return vals, idx
 
 
 def topk(x: torch.Tensor, K: int, vals: torch.Tensor | None = None,

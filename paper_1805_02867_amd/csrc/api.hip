@@ -28,9 +28,25 @@ struct ScratchSlot {
 constexpr int kScratchSlots = 64;
 constexpr size_t kScratchMin = 256 * 1024;
 
+// Fixed scratch of softmax_topk_ex_noalloc: one copy per device, held until
+// the process ends.  In host code `scratch` names a host-side stand-in, not
+// device memory: its device address is looked up once per device (with the
+// device current) and kept in DeviceState::scratch_ptr, which is what every
+// launch and copy uses.
+constexpr size_t kNoAllocBytes = OSM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+// Clears n 32-bit words (a kernel rather than a memset, so that a captured
+// graph replays it as an ordinary kernel node).
+__global__ void zero_u32(uint32_t* p, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0u;
+}
+
 struct DeviceState {
     std::once_flag once;
     int cus = 0;
+    void* scratch_ptr = nullptr;  // device address of `scratch` (null if the lookup failed)
     hipMemPool_t pool = nullptr;
     bool pool_ok = false;
     std::mutex mu;  // guards the scratch and counter tables
@@ -51,6 +67,8 @@ DeviceState* device_state(int* dev_out) {
             cus <= 0)
             cus = 256;
         s.cus = cus;
+        void* sp = nullptr;
+        if (hipGetSymbolAddress(&sp, HIP_SYMBOL(scratch)) == hipSuccess && sp) s.scratch_ptr = sp;
         // A library-owned stream-ordered pool keeps split-V scratch cheap to
         // allocate and free on any stream without touching the device's
         // default pool settings.
@@ -292,14 +310,14 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
     chunk = (chunk + E - 1) / E * E;
     S = (V + chunk - 1) / chunk;  // drop chunks that would start past the row
     if (N * S > kMaxDim) return OSM_EINVAL;
-    void* scratch = nullptr;
+    void* part = nullptr;
     bool temp = false;
     std::unique_lock<std::mutex> lk(ds->mu, std::defer_lock);  // held until the launches are in
-    const int st = acquire_scratch(ds, lk, stream, (size_t)N * (size_t)S * 8, &scratch, &temp);
+    const int st = acquire_scratch(ds, lk, stream, (size_t)N * (size_t)S * 8, &part, &temp);
     if (st != OSM_OK) return st;
-    hipError_t e = osm::launch_softmax_split(x, y, scratch, N, V, dtype, mode, S, chunk, vec,
+    hipError_t e = osm::launch_softmax_split(x, y, part, N, V, dtype, mode, S, chunk, vec,
                                              stream);
-    hipError_t f = temp ? hipFreeAsync(scratch, stream) : hipSuccess;
+    hipError_t f = temp ? hipFreeAsync(part, stream) : hipSuccess;
     if (e != hipSuccess) return OSM_EHIP;
     return hip_status(f);
 }
@@ -322,10 +340,12 @@ Plan choose_topk(int64_t N, int64_t V, int cus) {
     return {OSM_KERNEL_ROWS, 256};
 }
 
-// One top-k pass of variant `var` over x (already validated).
+// One top-k pass of variant `var` over x (already validated).  noalloc: the
+// split path's partials and row counters go to the device's fixed scratch
+// array instead of the stream's pool buffers.
 int launch_topk_pass(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
                      int dtype, int var, int kernel, int64_t param, DeviceState* ds,
-                     hipStream_t stream) {
+                     hipStream_t stream, bool noalloc = false) {
     Plan p = kernel == OSM_KERNEL_AUTO ? choose_topk(N, V, ds->cus) : Plan{kernel, param};
     osm::TopkLaunch a{x, vals, idx, nullptr, N, V, K, 1, 1, V, stream};
     if (p.kernel == OSM_KERNEL_ROWS) {
@@ -344,23 +364,37 @@ int launch_topk_pass(const void* x, float* vals, int32_t* idx, int64_t N, int64_
         a.waves_per_row = 4;
         return hip_status(osm::launch_topk(a, dtype, var));
     }
-    void* scratch = nullptr;
-    bool temp = false;
-    std::unique_lock<std::mutex> lk(ds->mu, std::defer_lock);  // held until the launch is in
-    int st = acquire_scratch(ds, lk, stream, osm::topk_part_bytes(N, S, K), &scratch, &temp);
-    if (st != OSM_OK) return st;
-    a.part = scratch;
     a.S = S;
     a.chunk = chunk;
+    if (noalloc) {
+        // partials first, then N row counters (256-byte aligned), cleared by a
+        // fill kernel in stream order before the split kernel
+        const size_t pb = (osm::topk_part_bytes(N, S, K) + 255) / 256 * 256;
+        if (pb + (size_t)N * 4 > kNoAllocBytes) return OSM_ESCRATCH;
+        if (!ds->scratch_ptr) return OSM_EHIP;
+        a.part = ds->scratch_ptr;
+        a.ctr = reinterpret_cast<uint32_t*>(static_cast<char*>(ds->scratch_ptr) + pb);
+        const int64_t blocks = (N + 255) / 256;
+        hipLaunchKernelGGL(zero_u32, dim3((unsigned)blocks), dim3(256), 0, stream, a.ctr, N);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return OSM_EHIP;
+        return hip_status(osm::launch_topk(a, dtype, var));
+    }
+    void* part = nullptr;
+    bool temp = false;
+    std::unique_lock<std::mutex> lk(ds->mu, std::defer_lock);  // held until the launch is in
+    int st = acquire_scratch(ds, lk, stream, osm::topk_part_bytes(N, S, K), &part, &temp);
+    if (st != OSM_OK) return st;
+    a.part = part;
     // per-row chunk counters: each row's last chunk merges it in the same kernel
     bool ctemp = false;
     st = acquire_counters(ds, lk, stream, (size_t)N, &a.ctr, &ctemp);
     if (st != OSM_OK) {
-        if (temp) (void)hipFreeAsync(scratch, stream);
+        if (temp) (void)hipFreeAsync(part, stream);
         return st;
     }
     hipError_t e = osm::launch_topk(a, dtype, var);
-    hipError_t f = temp ? hipFreeAsync(scratch, stream) : hipSuccess;
+    hipError_t f = temp ? hipFreeAsync(part, stream) : hipSuccess;
     hipError_t g = ctemp ? hipFreeAsync(a.ctr, stream) : hipSuccess;
     if (e != hipSuccess) return OSM_EHIP;
     if (f != hipSuccess) return hip_status(f);
@@ -374,7 +408,8 @@ bool topk_algo_ok(int algo) {
 }
 
 int run_topk(const void* x, void* y, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
-             int dtype, int algo, int kernel, int64_t param, hipStream_t stream) {
+             int dtype, int algo, int kernel, int64_t param, hipStream_t stream,
+             bool noalloc = false) {
     size_t bytes = 0;
     if (!check_shape(N, V, dtype, &bytes)) return OSM_EINVAL;
     if (K < 1 || K > OSM_TOPK_KMAX || (int64_t)K > V) return OSM_EINVAL;
@@ -405,7 +440,7 @@ int run_topk(const void* x, void* y, float* vals, int32_t* idx, int64_t N, int64
     switch (algo) {
         case OSM_TOPK_ONLINE_FUSED:
             return launch_topk_pass(x, vals, idx, N, V, K, dtype, osm::TK_ONLINE, kernel, param,
-                                    ds, stream);
+                                    ds, stream, noalloc);
         case OSM_TOPK_SAFE_FUSED:
             return launch_topk_pass(x, vals, idx, N, V, K, dtype, osm::TK_SAFE, kernel, param, ds,
                                     stream);
@@ -469,15 +504,15 @@ int run_proj_topk(const void* h, const void* w, float* vals, int32_t* idx, int64
     int64_t S = 1, tiles = 1;
     int parts = 2;
     osm::proj_topk_shape(N, V, K, ds->cus, &S, &tiles, &parts);
-    void* scratch = nullptr;
+    void* part = nullptr;
     bool temp = false;
     std::unique_lock<std::mutex> lk(ds->mu, std::defer_lock);  // held until the launches are in
-    st = acquire_scratch(ds, lk, stream, osm::proj_topk_part_bytes(N, S, parts, K), &scratch,
+    st = acquire_scratch(ds, lk, stream, osm::proj_topk_part_bytes(N, S, parts, K), &part,
                          &temp);
     if (st != OSM_OK) return st;
     hipError_t e =
-        osm::launch_proj_topk(h, w, vals, idx, scratch, N, H, V, K, S, tiles, parts, stream);
-    hipError_t f = temp ? hipFreeAsync(scratch, stream) : hipSuccess;
+        osm::launch_proj_topk(h, w, vals, idx, part, N, H, V, K, S, tiles, parts, stream);
+    hipError_t f = temp ? hipFreeAsync(part, stream) : hipSuccess;
     if (e != hipSuccess) return OSM_EHIP;
     return hip_status(f);
 }
@@ -512,6 +547,12 @@ int softmax_topk_ex(const void* x, float* vals, int32_t* idx, int64_t N, int64_t
                     int dtype, int kernel, int64_t param, hipStream_t stream) {
     return run_topk(x, nullptr, vals, idx, N, V, K, dtype, OSM_TOPK_ONLINE_FUSED, kernel, param,
                     stream);
+}
+
+int softmax_topk_ex_noalloc(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V,
+                            int K, int dtype, int kernel, int64_t param, hipStream_t stream) {
+    return run_topk(x, nullptr, vals, idx, N, V, K, dtype, OSM_TOPK_ONLINE_FUSED, kernel, param,
+                    stream, true);
 }
 
 int softmax_topk_algo(const void* x, void* y, float* vals, int32_t* idx, int64_t N, int64_t V,
@@ -597,6 +638,7 @@ const char* osm_status_string(int status) {
         case OSM_EUNSUPPORTED: return "unsupported configuration";
         case OSM_EHIP: return "HIP error while enqueuing work";
         case OSM_ENOMEM: return "scratch allocation failed";
+        case OSM_ESCRATCH: return "needs more than the fixed no-allocation scratch";
         default: return "unknown status";
     }
 }
