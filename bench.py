@@ -21,6 +21,8 @@ plain copy and a plain read as reference kernels.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        python bench.py --sweep FILE   (every workload shape and V sweep)
+       python bench.py --traffic-probe KEY   (one operation, for a counter pass)
+       python bench.py --traffic-summary DIR (counter passes -> profiles/traffic*)
 """
 from __future__ import annotations
 
@@ -225,6 +227,179 @@ def topk_probe(osm, synth):
     log("topk probe done")
 
 
+# HBM traffic: every operation of every workload, one operation per profiled
+# process (so that the counters of a process belong to one operation).
+# Workloads (synth.logits arguments) and the operations measured on them,
+# with the algorithmic bytes of one call (online and naive softmax: two loads
+# and one store per element; safe: three loads and one store; fused top-k: one
+# load per element and K (value, index) pairs per row).
+TRAFFIC_WORKLOADS = {
+    "4000x32000_f32": dict(N=4000, V=32000, sigma=2.0, dtype="f32", shift_frac=0.01),
+    "10x1000000_f32": dict(N=10, V=1_000_000, sigma=3.0, dtype="f32"),
+    "4000x50000_f32_ties": dict(N=4000, V=50000, sigma=2.0, dtype="f32", tie_frac=0.01),
+    "32768x128256_bf16": dict(N=32768, V=128256, sigma=4.0, dtype="bf16"),
+}
+TRAFFIC_OPS = [  # (key, workload, op, mode or K)
+    ("softmax_naive_4000x32000_f32", "4000x32000_f32", "softmax", "naive"),
+    ("softmax_safe_4000x32000_f32", "4000x32000_f32", "softmax", "safe"),
+    ("softmax_online_4000x32000_f32", "4000x32000_f32", "softmax", "online"),
+    ("topk5_4000x32000_f32", "4000x32000_f32", "topk", 5),
+    ("softmax_online_10x1000000_f32", "10x1000000_f32", "softmax", "online"),
+    ("topk5_10x1000000_f32", "10x1000000_f32", "topk", 5),
+    ("topk5_4000x50000_f32_ties", "4000x50000_f32_ties", "topk", 5),
+    ("topk10_4000x50000_f32_ties", "4000x50000_f32_ties", "topk", 10),
+    ("softmax_online_32768x128256_bf16", "32768x128256_bf16", "softmax", "online"),
+    ("softmax_safe_32768x128256_bf16", "32768x128256_bf16", "softmax", "safe"),
+    ("topk50_32768x128256_bf16", "32768x128256_bf16", "topk", 50),
+]
+TRAFFIC_CALLS = 3
+
+
+def traffic_algorithmic_bytes(wl: dict, op: str, arg) -> int:
+    es = 2 if wl["dtype"] == "bf16" else 4
+    n = wl["N"] * wl["V"]
+    if op == "softmax":
+        return (4 if arg == "safe" else 3) * es * n
+    return es * n + 8 * int(arg) * wl["N"]
+
+
+def traffic_probe(key: str):
+    """One operation of TRAFFIC_OPS (or `copy`: the plain 512 MB copy that
+    scales the counters), TRAFFIC_CALLS calls, for a counter pass."""
+    import torch
+    import paper_1805_02867_amd as osm
+    from paper_1805_02867_amd import synth
+    if key == "copy":
+        copy_probe()
+        return
+    ops = {k: (w, o, a) for k, w, o, a in TRAFFIC_OPS}
+    if key not in ops:
+        raise SystemExit(f"unknown traffic probe {key}; one of copy, {', '.join(ops)}")
+    w, op, arg = ops[key]
+    wl = dict(TRAFFIC_WORKLOADS[w])
+    N, V = wl.pop("N"), wl.pop("V")
+    x = synth.logits(N, V, seed=0, device="cuda", **wl)
+    if op == "softmax":
+        y = torch.empty_like(x)
+        for _ in range(TRAFFIC_CALLS):
+            osm.softmax_fwd(x, y, mode=arg)
+    else:
+        vals = torch.empty((N, arg), dtype=torch.float32, device="cuda")
+        idx = torch.empty((N, arg), dtype=torch.int32, device="cuda")
+        for _ in range(TRAFFIC_CALLS):
+            osm.softmax_topk(x, arg, vals, idx)
+    torch.cuda.synchronize()
+    log(f"traffic probe {key}: {TRAFFIC_CALLS} calls")
+
+
+def _counter_rows(d: str):
+    """(dispatch id, kernel, counter, value, start ns, end ns) from the
+    counter-collection CSV files of one rocprofv3 output directory."""
+    import csv
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    acc = {}
+    for fn in files:
+        with open(fn, newline="") as f:
+            for r in csv.DictReader(f):
+                name = r["Kernel_Name"].split("(")[0].strip()
+                if name.startswith("void "):
+                    name = name[5:]
+                key = (fn, r["Dispatch_Id"], name, r["Counter_Name"])
+                v = float(r["Counter_Value"])
+                s = int(r.get("Start_Timestamp") or 0)
+                e = int(r.get("End_Timestamp") or 0)
+                if key in acc:  # several instances of one counter: summed
+                    acc[key][0] += v
+                else:
+                    acc[key] = [v, s, e]
+    return [(k[1], k[2], k[3], v[0], v[1], v[2]) for k, v in acc.items()]
+
+
+def _per_kernel(d: str, counter: str):
+    """Per library kernel (osm::...): dispatches, median counter value and
+    median duration (ns) over its dispatches, in first-dispatch order."""
+    out = {}
+    for disp, name, cname, v, s, e in sorted(_counter_rows(d), key=lambda r: int(r[0])):
+        if cname != counter or not (name.startswith("osm::") or "copyBuffer" in name):
+            continue
+        out.setdefault(name, ([], []))
+        out[name][0].append(v)
+        out[name][1].append(e - s)
+    return {k: (len(v[0]), median(v[0]), median(v[1])) for k, v in out.items()}
+
+
+def traffic_summary(d: str):
+    """profiles/traffic.json and profiles/traffic_all_workloads.md from the
+    counter passes under d: <key>_fetch and <key>_write for every key of
+    TRAFFIC_OPS and for `copy` (rocprofv3 -d directories)."""
+    cf = _per_kernel(os.path.join(d, "copy_fetch"), "FETCH_SIZE")
+    cw = _per_kernel(os.path.join(d, "copy_write"), "WRITE_SIZE")
+    copy_bytes = N_ROWS * V_LEN * 4
+    (ck,) = [k for k in cf if "copyBuffer" in k]
+    fetch_scale = copy_bytes / (cf[ck][1] * 1024)
+    write_scale = copy_bytes / (cw[ck][1] * 1024)
+    sha = kernel_source_sha()
+    data = {"_scale": {"kernel": ck, "bytes": copy_bytes, "fetch_kib": cf[ck][1],
+                       "write_kib": cw[ck][1], "fetch_scale": fetch_scale,
+                       "write_scale": write_scale, "source_sha": sha}}
+    rows = []
+    for key, w, op, arg in TRAFFIC_OPS:
+        fk = _per_kernel(os.path.join(d, key + "_fetch"), "FETCH_SIZE")
+        wk = _per_kernel(os.path.join(d, key + "_write"), "WRITE_SIZE")
+        kernels = [k for k in fk if k.startswith("osm::")]
+        calls = TRAFFIC_CALLS
+        per = []
+        for k in kernels:
+            n, fkib, ns = fk[k]
+            wkib = wk.get(k, (0, 0.0, 0))[1]
+            per.append({"kernel": k, "dispatches_per_call": n / calls,
+                        "fetch_kib": fkib, "write_kib": wkib,
+                        "read_bytes": fkib * 1024 * fetch_scale,
+                        "write_bytes": wkib * 1024 * write_scale, "us": ns / 1e3})
+        rd = sum(p["read_bytes"] * p["dispatches_per_call"] for p in per)
+        wr = sum(p["write_bytes"] * p["dispatches_per_call"] for p in per)
+        us = sum(p["us"] * p["dispatches_per_call"] for p in per)
+        alg = traffic_algorithmic_bytes(TRAFFIC_WORKLOADS[w], op, arg)
+        data[key] = {"workload": w, "op": op, "arg": arg, "kernels": per,
+                     "read_bytes": rd, "write_bytes": wr, "bytes_per_launch": rd + wr,
+                     "algorithmic_bytes": alg, "us_under_counters": us, "source_sha": sha}
+        rows.append((key, per, rd, wr, alg, us))
+    with open(os.path.join(ROOT, "profiles", "traffic.json"), "w") as f:
+        json.dump(data, f, indent=1)
+    cmd = ("rocprofv3 --pmc {C} -d gpurun_out/traffic/{key}_{c} -o run -f csv -- "
+           "python3 bench.py --traffic-probe {key}")
+    lines = [
+        "# HBM traffic per call, every workload (rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE)", "",
+        "Each operation runs alone in its own process, {} calls; one counter per pass:".format(
+            TRAFFIC_CALLS), "",
+        "```",
+        cmd.format(C="FETCH_SIZE", c="fetch", key="<key>"),
+        cmd.format(C="WRITE_SIZE", c="write", key="<key>"),
+        "python3 bench.py --traffic-summary gpurun_out/traffic",
+        "```", "",
+        f"`<key>` is `copy` and each key below. Kernel sources hash: `{sha}`.", "",
+        f"Scale: a plain {copy_bytes / 1e6:.0f} MB copy (`{ck}`) reads FETCH_SIZE = "
+        f"{cf[ck][1]:.0f} KiB and WRITE_SIZE = {cw[ck][1]:.0f} KiB per dispatch, so bytes = "
+        f"FETCH_SIZE x 1024 x {fetch_scale:.4f} and WRITE_SIZE x 1024 x {write_scale:.4f}.",
+        "FETCH_SIZE counts what the L2 caches fetch over the fabric: reads served by the "
+        "256 MB last-level cache (MALL) count too, so `read` is an upper bound on HBM reads.",
+        "",
+        "Per call (medians over the calls' dispatches); `us` is the dispatch time while the "
+        "counters were collected (indicative only):", "",
+        "| key | kernels (dispatches per call) | read B | write B | algorithmic B | "
+        "(read+write)/alg | us | alg GB/s | fabric GB/s |",
+        "|---|---|---|---|---|---|---|---|---|"]
+    for key, per, rd, wr, alg, us in rows:
+        ks = "<br>".join(f"`{p['kernel']}` ({p['dispatches_per_call']:g})" for p in per)
+        lines.append(f"| {key} | {ks} | {rd:.4g} | {wr:.4g} | {alg:.4g} | {(rd + wr) / alg:.3f} | "
+                     f"{us:.1f} | {alg / us / 1e3:.0f} | {(rd + wr) / us / 1e3:.0f} |")
+    with open(os.path.join(ROOT, "profiles", "traffic_all_workloads.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    log("wrote profiles/traffic.json and profiles/traffic_all_workloads.md")
+
+
 def sweep(path: str):
     """Every workload shape, the paper's V sweeps at batch 4000 and 10, and
     its K sweep: one JSON record per (shape, op) into `path`.  Each record is
@@ -354,9 +529,16 @@ def main():
     ap.add_argument("--proj-probe", action="store_true")
     ap.add_argument("--topk-probe", action="store_true")
     ap.add_argument("--compare-reps", type=int, default=20)
+    ap.add_argument("--traffic-probe", metavar="KEY", help="one operation of one workload "
+                    "(or `copy`), for a counter pass")
+    ap.add_argument("--traffic-summary", metavar="DIR", help="write profiles/traffic.json "
+                    "and profiles/traffic_all_workloads.md from the counter passes under DIR")
     ap.add_argument("--sweep", metavar="FILE", help="time every workload shape and the V "
                     "sweeps; one JSON record per line into FILE")
     args = ap.parse_args()
+    if args.traffic_summary:
+        traffic_summary(args.traffic_summary)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(independent rows shard across GPUs with no communication)", file=sys.stderr)
@@ -378,6 +560,9 @@ def main():
         return
     if args.topk_probe:
         topk_probe(osm, synth)
+        return
+    if args.traffic_probe:
+        traffic_probe(args.traffic_probe)
         return
     if args.sweep:
         sweep(args.sweep)
