@@ -238,7 +238,10 @@ __global__ __launch_bounds__(BLOCK) void softmax_rows(const T* __restrict__ x, T
 // multiple of the 16-byte vector width, so when rows start aligned every
 // chunk does too.  Block b handles row b / S, chunk b % S.
 constexpr int SPLIT_BLOCK = 256;
-constexpr int SPLIT_U = 2;
+#ifndef OSM_SPLIT_U
+#define OSM_SPLIT_U 2
+#endif
+constexpr int SPLIT_U = OSM_SPLIT_U;
 
 __device__ __forceinline__ void chunk_bounds(int64_t c, int64_t chunk, int64_t V, int64_t& lo,
                                              int64_t& hi) {

@@ -815,10 +815,12 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_fused(const T* __restrict__ x,
 // wavefront per row.
 constexpr int TK_MERGE_B = 8;  // keys per lane in flight
 
-// One row by one wavefront: region holds region_slots(64 * B) slots, its
-// first K already empty; B keys per lane are in flight.  COH: the partials
-// are read with agent-scope atomic loads (written by other workgroups of the
-// same kernel).
+// One row by one wavefront: region holds at least region_slots(64) slots,
+// its first K already empty; B keys per lane are in flight, and the
+// selection trigger is checked after every 64 appended keys.  The pairs'
+// loads are issued with the first keys', so that a row of up to 64 B keys and
+// 64 chunks costs one round trip.  COH: the partials are read with
+// agent-scope atomic loads (written by other workgroups of the same kernel).
 template <int VAR, bool COH = false, int B = TK_MERGE_B>
 __device__ __forceinline__ void topk_merge_row(uint64_t* region, const uint64_t* pkeys,
                                                const MD* pmd, float* __restrict__ vals,
@@ -829,8 +831,21 @@ __device__ __forceinline__ void topk_merge_row(uint64_t* region, const uint64_t*
     const int fa = flush_at(K);
     const int64_t n = S * K;
     const uint64_t* pk = pkeys + row * n;
-    for (int64_t c = 0; c < n; c += 64 * B) {
-        uint64_t k[B];
+    const MD* pm = pmd + row * S;
+    auto load_md = [&](int64_t j) {
+        if constexpr (COH)
+            return __builtin_bit_cast(MD, __hip_atomic_load(reinterpret_cast<const uint64_t*>(pm + j),
+                                                            __ATOMIC_RELAXED,
+                                                            __HIP_MEMORY_SCOPE_AGENT));
+        else
+            return pm[j];
+    };
+    // the first pair of this lane (chunk `lane`), requested before the keys
+    MD md = md_empty();
+    if constexpr (VAR != TK_VALUES) {
+        if (lane < S) md = load_md(lane);
+    }
+    auto load_keys = [&](uint64_t (&k)[B], int64_t c) {
 #pragma unroll
         for (int b = 0; b < B; ++b) {
             const int64_t j = c + b * 64 + lane;
@@ -840,24 +855,31 @@ __device__ __forceinline__ void topk_merge_row(uint64_t* region, const uint64_t*
             else
                 k[b] = j < n ? pk[j] : 0ull;
         }
+    };
+    uint64_t key;
+    if (n <= 64 * B && K <= TK_ROUNDS_MAX) {
+        // every key in registers at once: K rounds of the wavefront maximum
+        // below the last key taken (0 marks a missing key and is never taken)
+        uint64_t k[B];
+        load_keys(k, 0);
+        int found;
+        key = select_topk<B>(k, B, K, &found);
+    } else {
+        for (int64_t c = 0; c < n; c += 64 * B) {
+            uint64_t k[B];
+            load_keys(k, c);
 #pragma unroll
-        for (int b = 0; b < B; ++b) tw.append(k[b] > tw.tau, k[b]);  // 0 never passes
-        if (tw.qcount >= fa) tw.flush();
-    }
-    tw.flush();
-    const uint64_t key = tw.mine;
-    MD md = md_empty();
-    if constexpr (VAR != TK_VALUES) {
-        for (int64_t j = lane; j < S; j += 64) {
-            MD p;
-            if constexpr (COH)
-                p = __builtin_bit_cast(MD, __hip_atomic_load(
-                                               reinterpret_cast<const uint64_t*>(pmd + row * S + j),
-                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-            else
-                p = pmd[row * S + j];
-            md = md_merge(md, p);
+            for (int b = 0; b < B; ++b) {
+                tw.append(k[b] > tw.tau, k[b]);  // 0 never passes
+                if (tw.qcount >= fa) tw.flush();
+            }
         }
+        tw.flush();
+        key = tw.mine;
+    }
+    if constexpr (VAR != TK_VALUES) {
+        // chunks lane, lane + 64, ... in order, then the butterfly
+        for (int64_t j = lane + 64; j < S; j += 64) md = md_merge(md, load_md(j));
         md = group_merge<64>(md);  // every lane takes part
     }
     if (lane < K) {
@@ -878,7 +900,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_merge(const uint64_t* __restric
                                                       int32_t* __restrict__ idx, int64_t N,
                                                       int64_t S, int K) {
     constexpr int WB = TK_BLOCK / 64;
-    constexpr int REGION = region_slots(64 * TK_MERGE_B);
+    constexpr int REGION = region_slots(64);
     __shared__ uint64_t region[WB][REGION];
     const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t row = (int64_t)blockIdx.x * WB + wv;
@@ -900,11 +922,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_split1(const T* __restrict__ x,
                                                        MD* __restrict__ pmd, uint32_t* ctr,
                                                        int64_t N, int64_t V, int K, int64_t seg,
                                                        int64_t segs) {
-    // keys per lane the merge keeps in flight: as many as the region holds
-    constexpr int MB = (topk_region<T, U>() - region_slots(0)) / 64 < TK_MERGE_B
-                           ? (topk_region<T, U>() - region_slots(0)) / 64
-                           : TK_MERGE_B;
-    static_assert(MB >= 1, "merge fits the region");
+    static_assert(topk_region<T, U>() >= region_slots(64), "the merge appends 64 keys per check");
     __shared__ TopkSmem<T, U> sm;
     const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t vr = blockIdx.x;
@@ -925,7 +943,7 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_split1(const T* __restrict__ x,
     // every chunk of the row is in: its partials are read at the coherence
     // point, after the count that says so
     if (lane < K) sm.region[wv][lane] = 0;
-    topk_merge_row<VAR, true, MB>(sm.region[wv], pkeys, pmd, vals, idx, row, segs, K);
+    topk_merge_row<VAR, true>(sm.region[wv], pkeys, pmd, vals, idx, row, segs, K);
     if (lane == 0) __hip_atomic_store(ctr + row, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
