@@ -23,6 +23,8 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        python bench.py --sweep FILE   (every workload shape and V sweep)
        python bench.py --traffic-probe KEY   (one operation, for a counter pass)
        python bench.py --traffic-summary DIR (counter passes -> profiles/traffic*)
+       python bench.py --sweep-summary FILE  (sweep records -> profiles/sweep_all_workloads.md)
+       python bench.py --kernel-stats DIR OUT COMMAND (rocprofv3 statistics -> profiles/OUT)
 """
 from __future__ import annotations
 
@@ -400,6 +402,132 @@ def traffic_summary(d: str):
     log("wrote profiles/traffic.json and profiles/traffic_all_workloads.md")
 
 
+def sweep_summary(path: str):
+    """profiles/sweep_all_workloads.md from the JSON records of `--sweep`."""
+    recs = [json.loads(l) for l in open(path) if l.strip()]
+    by = {}
+    for r in recs:
+        by.setdefault(r["workload"], {})[r["op"]] = r
+    named = [w for w in by if not w.startswith("sweep_") and not w.startswith("proj_")]
+    L = ["# All workload shapes, the V sweeps and the K sweep (bench.py --sweep)", "",
+         "Commands (repository root, GPU host): `python bench.py --sweep <file>`, then "
+         "`python bench.py --sweep-summary <file>`.", "",
+         "Each entry is the median over 10 batches of back-to-back calls through the Python "
+         "binding, each batch queued behind a ~4 ms spin kernel so that the events bracket GPU "
+         "time, not the host's call rate. GB/s are algorithmic: softmax naive/online 12 B/elem "
+         "(binary32) or 6 (bfloat16), safe 16 or 8, resident 8 or 4; fused top-k 4 or 2 B/elem "
+         "+ 8 B per output pair. Peak = 8000 GB/s.", "",
+         "## Workload shapes", "",
+         "| workload | op | plan | us | GB/s | % of 8 TB/s |", "|---|---|---|---|---|---|"]
+    for w in named:
+        for op, r in by[w].items():
+            if op.endswith("_cold") or "GBps" not in r or op.startswith("topk_") and \
+                    not op.startswith("topk_fused"):
+                continue
+            L.append(f"| {w} | {op} | {r.get('plan', '')} | {r['us']} | {r['GBps']} | "
+                     f"{r['GBps'] / PEAK_HBM_GBS * 100:.1f} |")
+    L += ["", "## Cold caches", "",
+          "Inputs that fit in the 256 MB last-level cache, timed again with a 512 MB buffer "
+          "read (torch sum: ordinary loads, so it evicts without dirty lines) before each call "
+          "(events around the call alone, calls queued behind a spin kernel; median of 20). "
+          "Warm = the back-to-back figure; an isolated call also carries ~3 us of dispatch "
+          "that back-to-back calls hide.", "",
+          "| workload | online softmax warm us | cold us | cold GB/s (% of 8 TB/s) | "
+          "fused top-5 warm us | cold us | cold GB/s (%) |", "|---|---|---|---|---|---|---|"]
+    for w, ops in by.items():
+        if "softmax_online_cold" not in ops:
+            continue
+        sc, tc = ops["softmax_online_cold"], ops.get("topk_fused_k5_cold")
+        tw = ops.get("topk_fused_k5", ops.get("topk_online_fused_k5", {}))
+        L.append(f"| {w} | {ops['softmax_online']['us']} | {sc['us']} | {sc['GBps']} "
+                 f"({sc['GBps'] / PEAK_HBM_GBS * 100:.1f}) | {tw.get('us', '')} | "
+                 f"{tc['us'] if tc else ''} | "
+                 + (f"{tc['GBps']} ({tc['GBps'] / PEAK_HBM_GBS * 100:.1f}) |" if tc else " |"))
+    L += ["", "## Softmax + top-k algorithms (Section 5.2's comparison), K = 5", "",
+          "Times in us; ratio = safe unfused / online fused (the paper's Fig. 3 and 4 quantity).",
+          "", "| workload | V | online fused | safe fused | online unfused | safe unfused | "
+          "ratio | top-k plan |", "|---|---|---|---|---|---|---|---|"]
+    for w, ops in by.items():
+        if "topk_ratios_k5" not in ops:
+            continue
+        t = {a: ops[f"topk_{a}_k5"]["us"] for a in
+             ("online_fused", "safe_fused", "online_unfused", "safe_unfused")}
+        r = ops["topk_ratios_k5"]
+        L.append(f"| {w} | {r['V']} | {t['online_fused']} | {t['safe_fused']} | "
+                 f"{t['online_unfused']} | {t['safe_unfused']} | "
+                 f"{r['safe_unfused_over_online_fused']} | {r['topk_plan']} |")
+    L += ["", "## K sweep (ratio safe unfused / online fused)", "",
+          "| workload | K | online fused us | safe unfused us | ratio |", "|---|---|---|---|---|"]
+    for w, ops in by.items():
+        ks = sorted(int(op[len("topk_ratios_k"):]) for op in ops if op.startswith("topk_ratios_k"))
+        if len(ks) < 2:
+            continue
+        for K in ks:
+            L.append(f"| {w} | {K} | {ops[f'topk_online_fused_k{K}']['us']} | "
+                     f"{ops[f'topk_safe_unfused_k{K}']['us']} | "
+                     f"{ops[f'topk_ratios_k{K}']['safe_unfused_over_online_fused']} |")
+    L += ["", "## Softmax V sweeps (elements/s; ratio = safe / online time)", "",
+          "resident = the row-resident variant (one load + one store per element), reported "
+          "apart.", "", "| workload | V | online us | safe us | naive us | resident us | "
+          "online elem/s | safe/online |", "|---|---|---|---|---|---|---|---|"]
+    for w, ops in by.items():
+        if not w.startswith("sweep_") or "softmax_online" not in ops:
+            continue
+        o = ops["softmax_online"]
+        res = ops.get("softmax_resident", {}).get("us", "")
+        L.append(f"| {w} | {o['V']} | {o['us']} | {ops['softmax_safe']['us']} | "
+                 f"{ops['softmax_naive']['us']} | {res} | {o['elements_per_s']:.3g} | "
+                 f"{ops['softmax_safe']['us'] / o['us']:.3f} |")
+    L += ["", "## Projection with softmax + top-5 in its epilogue (bfloat16 h, W; binary32 "
+          "accumulation)", "",
+          "fused = proj_softmax_topk (logits never written); proj_then_topk = proj_fwd writing "
+          "binary32 logits, then the fused top-k over them; library = torch's bfloat16 matmul "
+          "(hipBLASLt) then the fused top-k over bfloat16 logits. TF/s = 2 N H V / time; the "
+          "bfloat16 dense peak is 2500 TF/s.", "",
+          "| N x H x V | fused us | fused TF/s | proj_fwd us (TF/s) | proj_then_topk us | "
+          "library_gemm_then_topk us |", "|---|---|---|---|---|---|"]
+    for w, ops in by.items():
+        if not w.startswith("proj_"):
+            continue
+        r = ops["proj_softmax_topk_k5"]
+        L.append(f"| {r['N']} x {r['H']} x {r['V']} | {r['fused_us']} | {r['fused_TFLOPs']} | "
+                 f"{r['proj_only_us']} ({r['proj_only_TFLOPs']}) | {r['proj_then_topk_us']} | "
+                 f"{r['library_gemm_then_topk_us']} |")
+    with open(os.path.join(ROOT, "profiles", "sweep_all_workloads.md"), "w") as f:
+        f.write("\n".join(L) + "\n")
+    log("wrote profiles/sweep_all_workloads.md")
+
+
+def kernel_stats_summary(d: str, out_name: str, command: str):
+    """A markdown table of rocprofv3's kernel statistics (--kernel-trace --stats)
+    found under d, written to profiles/<out_name>."""
+    import csv
+    files = glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_stats.csv under {d}")
+    rows = []
+    with open(files[0], newline="") as f:
+        for r in csv.DictReader(f):
+            name = r["Name"].split("(")[0].strip()
+            if name.startswith("void "):
+                name = name[5:]
+            rows.append((name, int(r["Calls"]), float(r["AverageNs"]) / 1e3,
+                         float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
+                         float(r["Percentage"])))
+    rows.sort(key=lambda r: -r[5])
+    L = [f"# Kernel time (rocprofv3 --kernel-trace --stats)", "", "Command (repository root, GPU "
+         "host), then the summary:", "", "```", command,
+         f"python3 bench.py --kernel-stats <out> {out_name} '<the command above>'", "```", "",
+         f"Kernel sources hash: `{kernel_source_sha()}`",
+         "", "| kernel | calls | average us | min us | max us | share % |",
+         "|---|---|---|---|---|---|"]
+    for name, n, avg, mn, mx, pc in rows[:25]:
+        L.append(f"| `{name}` | {n} | {avg:.2f} | {mn:.2f} | {mx:.2f} | {pc:.1f} |")
+    with open(os.path.join(ROOT, "profiles", out_name), "w") as f:
+        f.write("\n".join(L) + "\n")
+    log(f"wrote profiles/{out_name}")
+
+
 def sweep(path: str):
     """Every workload shape, the paper's V sweeps at batch 4000 and 10, and
     its K sweep: one JSON record per (shape, op) into `path`.  Each record is
@@ -533,11 +661,21 @@ def main():
                     "(or `copy`), for a counter pass")
     ap.add_argument("--traffic-summary", metavar="DIR", help="write profiles/traffic.json "
                     "and profiles/traffic_all_workloads.md from the counter passes under DIR")
+    ap.add_argument("--sweep-summary", metavar="FILE", help="write "
+                    "profiles/sweep_all_workloads.md from the records of --sweep")
+    ap.add_argument("--kernel-stats", nargs=3, metavar=("DIR", "OUT", "COMMAND"),
+                    help="write profiles/OUT from the rocprofv3 kernel statistics under DIR")
     ap.add_argument("--sweep", metavar="FILE", help="time every workload shape and the V "
                     "sweeps; one JSON record per line into FILE")
     args = ap.parse_args()
     if args.traffic_summary:
         traffic_summary(args.traffic_summary)
+        return
+    if args.sweep_summary:
+        sweep_summary(args.sweep_summary)
+        return
+    if args.kernel_stats:
+        kernel_stats_summary(*args.kernel_stats)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
