@@ -332,12 +332,19 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
 // is split into chunks (a workgroup each, about two workgroups per CU in all:
 // every chunk pays a fixed selection cost, so more, shorter chunks stop
 // paying off early); otherwise a workgroup (four wavefronts) per row.
-Plan choose_topk(int64_t N, int64_t V, int cus) {
+//
+// The chunk count is also capped so that a row's S * K partial keys fit the
+// merge's single register batch (512 keys; a larger merge goes through the
+// queue and its repeated selections: 4 x 10^6 top-5 took 20.8 us at 128
+// chunks against 15.7 at 52).
+Plan choose_topk(int64_t N, int64_t V, int K, int cus) {
     if (N >= 4 * (int64_t)cus || V <= 1536) return {OSM_KERNEL_ROWS, 64};
     if (N < 2 * (int64_t)cus && V >= 8192) {
         int64_t S = (2 * (int64_t)cus + N - 1) / N;
         int64_t s_cap = V / 4096;  // keep chunks >= 4096 elements
         if (S > s_cap) S = s_cap;
+        const int64_t k_cap = 512 / K;
+        if (S > k_cap) S = k_cap;
         if (S >= 2) return {OSM_KERNEL_SPLIT, S};
     }
     return {OSM_KERNEL_ROWS, 256};
@@ -349,7 +356,7 @@ Plan choose_topk(int64_t N, int64_t V, int cus) {
 int launch_topk_pass(const void* x, float* vals, int32_t* idx, int64_t N, int64_t V, int K,
                      int dtype, int var, int kernel, int64_t param, DeviceState* ds,
                      hipStream_t stream, bool noalloc = false) {
-    Plan p = kernel == OSM_KERNEL_AUTO ? choose_topk(N, V, ds->cus) : Plan{kernel, param};
+    Plan p = kernel == OSM_KERNEL_AUTO ? choose_topk(N, V, K, ds->cus) : Plan{kernel, param};
     osm::TopkLaunch a{x, vals, idx, nullptr, N, V, K, 1, 1, V, stream};
     if (p.kernel == OSM_KERNEL_ROWS) {
         a.waves_per_row = (int)(p.param / 64);
@@ -575,7 +582,7 @@ int osm_topk_plan(int64_t N, int64_t V, int dtype, int K, int* kernel, int64_t* 
     if (K < 1 || K > OSM_TOPK_KMAX || (int64_t)K > V) return OSM_EINVAL;
     if (!kernel || !param) return OSM_EINVAL;
     DeviceState* ds = device_state(nullptr);
-    Plan p = choose_topk(N, V, ds ? ds->cus : 256);
+    Plan p = choose_topk(N, V, K, ds ? ds->cus : 256);
     *kernel = p.kernel;
     *param = p.param;
     return OSM_OK;
