@@ -184,12 +184,14 @@ __device__ __forceinline__ void pj_mma(const uint16_t (&xt)[C::TX][PJ_BK],
 }
 
 // Stage hand-over.  The loads of the next stage were issued one step
-// earlier; each thread waits for its own, then the workgroup barrier makes
-// every thread's loads visible and tells that every wavefront has finished
-// reading the stage about to be refilled.  (A plain s_barrier: the fenced
+// earlier; each thread waits for its own, and for its own fragment reads of
+// the stage about to be refilled (the compiler may leave the last of them
+// in flight, their products scheduled after the barrier), then the
+// workgroup barrier makes every thread's loads visible and tells that every
+// wavefront has finished reading that stage.  (A plain s_barrier: the fenced
 // __syncthreads would also make the compiler wait for everything else.)
 __device__ __forceinline__ void pj_handover() {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 }
