@@ -254,6 +254,7 @@ __device__ __forceinline__ void pj_run(const uint16_t* __restrict__ X, int64_t n
             pj_mma<C>(sm.st[1].x, sm.st[1].y, xo, yo, acc);
         }
         // every wavefront's last read of stage 1 is done before epi may write it
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         epi(t, x0, y0, acc);
