@@ -528,6 +528,148 @@ def kernel_stats_summary(d: str, out_name: str, command: str):
     log(f"wrote profiles/{out_name}")
 
 
+# Core counters of the fused top-k and of the projection kernels: a kernel
+# trace and two counter passes per probe (each pass its own process, within
+# the per-block counter limits), summarised by `--counters-summary KIND DIR`
+# from DIR/stats, DIR/p0 and DIR/p1.
+CORE_COUNTERS = {
+    "topk": ("--topk-probe", "topk_fused_counters.md",
+             ["SQ_WAVE_CYCLES SQ_BUSY_CU_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_VALU "
+              "SQ_INSTS_VALU SQ_INSTS_LDS GRBM_GUI_ACTIVE",
+              "SQ_ACTIVE_INST_ANY SQ_INSTS_VMEM_RD SQ_INSTS_SALU SQ_WAVES GRBM_COUNT"]),
+    "proj": ("--proj-probe", "proj_4000x4096x128256_bf16.md",
+             ["SQ_WAVE_CYCLES SQ_BUSY_CU_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY "
+              "SQ_VALU_MFMA_BUSY_CYCLES SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_INSTS_LDS "
+              "GRBM_GUI_ACTIVE",
+              "SQ_INSTS_MFMA SQ_INSTS_VALU SQ_INSTS_VMEM_RD TCC_HIT_sum TCC_MISS_sum GRBM_COUNT"]),
+}
+# the fused top-k probe's cases, in dispatch order, three calls each
+TOPK_PROBE_CASES = [("4000x32000 f32", 4000, 32000, 4, 5), ("4000x32000 f32", 4000, 32000, 4, 50),
+                    ("32768x128256 bf16", 32768, 128256, 2, 5),
+                    ("32768x128256 bf16", 32768, 128256, 2, 50)]
+
+
+def _trace_dispatches(d: str):
+    """(kernel, duration ns) of every dispatch in a kernel trace under d, in
+    dispatch order."""
+    import csv
+    files = glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_trace.csv under {d}")
+    out = []
+    with open(files[0], newline="") as f:
+        for r in csv.DictReader(f):
+            name = r["Kernel_Name"].split("(")[0].strip()
+            if name.startswith("void "):
+                name = name[5:]
+            out.append((int(r["Dispatch_Id"]), name,
+                        int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+    out.sort()
+    return [(n, t) for _, n, t in out]
+
+
+def _dispatch_counters(d: str, keep):
+    """Counter values per dispatch (dict counter -> value) of the kernels
+    whose name passes `keep`, in dispatch order."""
+    per = {}
+    for disp, name, cname, v, s, e in _counter_rows(d):
+        if keep(name):
+            per.setdefault(int(disp), (name, {}))[1][cname] = v
+    return [per[k] for k in sorted(per)]
+
+
+def counters_summary(kind: str, d: str):
+    """profiles/<file> for the core counters of `kind` ('topk' or 'proj')
+    from the kernel trace d/stats and the counter passes d/p0, d/p1."""
+    probe, out_name, passes = CORE_COUNTERS[kind]
+    cmds = [f"rocprofv3 --kernel-trace --stats -f csv -d <out>/stats -o run -- python3 bench.py "
+            f"{probe}"]
+    cmds += [f"rocprofv3 --pmc {c} -d <out>/p{i} -o run -f csv -- python3 bench.py {probe}"
+             for i, c in enumerate(passes)]
+    cmds.append(f"python3 bench.py --counters-summary {kind} <out>")
+    trace = _trace_dispatches(os.path.join(d, "stats"))
+    pcs = [_dispatch_counters(os.path.join(d, f"p{i}"), lambda n: n.startswith("osm::"))
+           for i in range(len(passes))]
+
+    def merged(i):  # counters of the i-th library dispatch, over both passes
+        c, name = {}, None
+        for p in pcs:
+            name = p[i][0]
+            c.update(p[i][1])
+        return name, c
+
+    L = []
+    if kind == "topk":
+        L += ["# Fused softmax + top-k: kernel time and core counters", "",
+              "Commands (repository root, GPU host; each counter pass its own process):", "",
+              "```", *cmds, "```", "", f"Kernel sources hash: `{kernel_source_sha()}`", "",
+              "Three calls per case, in the order below (one wavefront per row). VALU busy =",
+              "SQ_ACTIVE_INST_VALU / (4 SIMDs x SQ_BUSY_CU_CYCLES); waiting = SQ_WAIT_ANY / "
+              "SQ_WAVE_CYCLES",
+              "(wave cycles spent on a dependency, mostly `s_waitcnt` for loads); VALU and LDS "
+              "instructions per",
+              "element = wavefront instructions x 64 / elements; time from the kernel trace "
+              "(median of the three).", "",
+              "| case | K | kernel | us | GB/s | VALU busy | waiting | VALU instr / element | "
+              "LDS instr / element |", "|---|---|---|---|---|---|---|---|---|"]
+        tk = [t for n, t in trace if n.startswith("osm::topk_fused")]
+        for ci, (case, N, V, es, K) in enumerate(TOPK_PROBE_CASES):
+            us = median(tk[3 * ci:3 * ci + 3]) / 1e3
+            rows = [merged(3 * ci + j) for j in range(3)]
+            name = rows[0][0]
+            m = {c: median([r[1][c] for r in rows]) for c in rows[0][1]}
+            busy = m["SQ_ACTIVE_INST_VALU"] / (4 * m["SQ_BUSY_CU_CYCLES"])
+            wait = m["SQ_WAIT_ANY"] / m["SQ_WAVE_CYCLES"]
+            L.append(f"| {case} | {K} | `{name}` | {us:.1f} | {N * V * es / us / 1e3:.0f} | "
+                     f"{100 * busy:.1f}% | {100 * wait:.1f}% | "
+                     f"{m['SQ_INSTS_VALU'] * 64 / (N * V):.2f} | "
+                     f"{m['SQ_INSTS_LDS'] * 64 / (N * V):.3f} |")
+    else:
+        N, H, V = 4000, 4096, 128256
+        L += ["# Projection kernels at 4000 x 4096 x 128256 (bfloat16 h, w; binary32 "
+              "accumulation)", "",
+              "Commands (repository root, GPU host; each counter pass its own process):", "",
+              "```", *cmds, "```", "", f"Kernel sources hash: `{kernel_source_sha()}`", "",
+              "## Kernel time (3 calls of each entry point, from the kernel trace)", "",
+              "| kernel | calls | avg us | min us | max us | TF/s at avg (2NHV) |",
+              "|---|---|---|---|---|---|"]
+        by = {}
+        for n, t in trace:
+            if n.startswith("osm::"):
+                by.setdefault(n, []).append(t / 1e3)
+        for n, ts in by.items():
+            avg = sum(ts) / len(ts)
+            tf = f"{2.0 * N * H * V / avg / 1e6:.0f}" if n.startswith("osm::proj") else ""
+            L.append(f"| `{n}` | {len(ts)} | {avg:.1f} | {min(ts):.1f} | {max(ts):.1f} | {tf} |")
+        L += ["", "## Counters per dispatch (medians over the three calls)", "",
+              "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x SQ_BUSY_CU_CYCLES); clock = "
+              "GRBM_GUI_ACTIVE / 8 XCDs / kernel time (kernel time from the trace above).", "",
+              "| kernel | MFMA busy | clock GHz | LDS bank conflict / LDS active cycles | "
+              "waves waiting on counters / wave cycles | L2 hit rate |",
+              "|---|---|---|---|---|---|"]
+        rows = [merged(i) for i in range(len(pcs[0]))]
+        names = []
+        for n, _ in rows:
+            if n.startswith("osm::proj") and n not in names:
+                names.append(n)
+        for n in names:
+            rs = [c for nn, c in rows if nn == n]
+            m = {c: median([r[c] for r in rs]) for c in rs[0]}
+            avg_ns = sum(by[n]) / len(by[n]) * 1e3
+            mfma = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (4 * m["SQ_BUSY_CU_CYCLES"])
+            clk = m["GRBM_GUI_ACTIVE"] / 8 / avg_ns
+            bank = m["SQ_LDS_BANK_CONFLICT"] / max(m["SQ_LDS_IDX_ACTIVE"], 1.0)
+            wait = m["SQ_WAIT_ANY"] / m["SQ_WAVE_CYCLES"]
+            hit = m["TCC_HIT_sum"] / max(m["TCC_HIT_sum"] + m["TCC_MISS_sum"], 1.0)
+            L.append(f"| `{n}` | {100 * mfma:.1f}% | {clk:.2f} | {bank:.3f} | {100 * wait:.1f}% "
+                     f"| {100 * hit:.1f}% |")
+        L += ["", "The clock figure is taken under the profiler (one dispatch at a time).",
+              "hipBLASLt's GEMM on the same shape (bfloat16 out) runs at ~1.42 PF/s."]
+    with open(os.path.join(ROOT, "profiles", out_name), "w") as f:
+        f.write("\n".join(L) + "\n")
+    log(f"wrote profiles/{out_name}")
+
+
 def sweep(path: str):
     """Every workload shape, the paper's V sweeps at batch 4000 and 10, and
     its K sweep: one JSON record per (shape, op) into `path`.  Each record is
@@ -655,6 +797,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--proj-probe", action="store_true")
+    ap.add_argument("--counters-summary", nargs=2, metavar=("KIND", "DIR"),
+                    help="write the core-counter summary of KIND (topk or proj) from the "
+                         "rocprofv3 outputs DIR/stats, DIR/p0 and DIR/p1")
     ap.add_argument("--topk-probe", action="store_true")
     ap.add_argument("--compare-reps", type=int, default=20)
     ap.add_argument("--traffic-probe", metavar="KEY", help="one operation of one workload "
@@ -676,6 +821,9 @@ def main():
         return
     if args.kernel_stats:
         kernel_stats_summary(*args.kernel_stats)
+        return
+    if args.counters_summary:
+        counters_summary(*args.counters_summary)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
