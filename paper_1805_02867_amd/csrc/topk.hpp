@@ -153,13 +153,15 @@ __device__ __forceinline__ uint64_t xor_partner_key(uint64_t k) {
 
 // One compare-exchange stage: the lower lane of each pair keeps the larger
 // key when `desc_block` holds, the smaller one otherwise (and the upper lane
-// the other one).
+// the other one).  A lane that keeps the larger key takes its partner's when
+// that is larger, one that keeps the smaller takes it when it is not larger
+// (equal keys are the same key either way): one compare and one mask xor,
+// where a select between two compares became masked control flow.
 template <int J>
 __device__ __forceinline__ uint64_t cx_stage(uint64_t v, bool desc_block) {
     const uint64_t p = xor_partner_key<J>(v);
     const bool lower = (__lane_id() & J) == 0;
-    const bool keep_max = lower == desc_block;
-    const bool take = keep_max ? (p > v) : (p < v);
+    const bool take = (p > v) != (lower != desc_block);
     return take ? p : v;
 }
 
