@@ -114,10 +114,14 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     }
 }
 
+// The butterflies leave the maximum in every lane; it is read from the first
+// lane so that the compiler holds it as a scalar (callers run with every
+// lane of the wavefront active), and a test on it is a scalar branch.
 __device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
     const uint32_t hi = (uint32_t)(k >> 32), lo = (uint32_t)k;
-    const uint32_t mh = wave_max_u32(hi);
-    const uint32_t ml = wave_max_u32(hi == mh ? lo : 0u);
+    const uint32_t mh = (uint32_t)__builtin_amdgcn_readfirstlane((int)wave_max_u32(hi));
+    const uint32_t ml =
+        (uint32_t)__builtin_amdgcn_readfirstlane((int)wave_max_u32(hi == mh ? lo : 0u));
     return ((uint64_t)mh << 32) | ml;
 }
 
