@@ -956,14 +956,14 @@ __global__ __launch_bounds__(TK_BLOCK) void topk_split1(const T* __restrict__ x,
 // 16-byte vectors per lane per step, by shape and element type: enough
 // loads in flight per wavefront without pushing the register count (and so
 // the occupancy) down; bfloat16 vectors widen to twice the registers.  For
-// bfloat16 rows of a wavefront, four vectors (32 elements a lane per step,
-// 114 registers, four wavefronts per SIMD) also give the first step's lane
-// maxima, and so the starting threshold, twice the reach of two.
+// bfloat16 rows of a wavefront, six vectors (48 elements a lane per step,
+// 146 registers, three wavefronts per SIMD) also give the first step's lane
+// maxima, and so the starting threshold, three times the reach of two.
 #ifndef OSM_TOPK_U1
 #define OSM_TOPK_U1 5
 #endif
 #ifndef OSM_TOPK_U1B
-#define OSM_TOPK_U1B 4
+#define OSM_TOPK_U1B 6
 #endif
 #ifndef OSM_TOPK_U2
 #define OSM_TOPK_U2 4
