@@ -329,9 +329,12 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
 // SIMD several wavefronts, or when rows are short (up to 1536 elements: a
 // wavefront streams them in a step or two, and more wavefronts per row only
 // add the barrier and the cross-wavefront merge); a small batch of long rows
-// is split into chunks (a workgroup each, about two workgroups per CU in all:
-// every chunk pays a fixed selection cost, so more, shorter chunks stop
-// paying off early); otherwise a workgroup (four wavefronts) per row.
+// is split into chunks (a workgroup each, at most two workgroups per CU in
+// all, at least two chunks a row: every chunk pays a fixed selection cost, so
+// more, shorter chunks stop paying off early, and a third workgroup on a few
+// CUs slows their chunks, which the rows then wait for: 10 x 4e6 top-5 took
+// 34.5 us in 510 workgroups against 41.8 in 520); otherwise a workgroup (four
+// wavefronts) per row.
 //
 // The chunk count is also capped so that a row's S * K partial keys fit the
 // merge's single register batch (512 keys; a larger merge goes through the
@@ -340,7 +343,8 @@ int run_softmax(const void* x, void* y, int64_t N, int64_t V, int dtype, int mod
 Plan choose_topk(int64_t N, int64_t V, int K, int cus) {
     if (N >= 4 * (int64_t)cus || V <= 1536) return {OSM_KERNEL_ROWS, 64};
     if (N < 2 * (int64_t)cus && V >= 8192) {
-        int64_t S = (2 * (int64_t)cus + N - 1) / N;
+        int64_t S = (2 * (int64_t)cus) / N;
+        if (S < 2) S = 2;
         int64_t s_cap = V / 4096;  // keep chunks >= 4096 elements
         if (S > s_cap) S = s_cap;
         const int64_t k_cap = 512 / K;
