@@ -370,7 +370,7 @@ def traffic_summary(d: str):
         rows.append((key, per, rd, wr, alg, us))
     with open(os.path.join(ROOT, "profiles", "traffic.json"), "w") as f:
         json.dump(data, f, indent=1)
-    cmd = ("rocprofv3 --pmc {C} -d gpurun_out/traffic/{key}_{c} -o run -f csv -- "
+    cmd = ("rocprofv3 --pmc {C} -d <out>/{key}_{c} -o run -f csv -- "
            "python3 bench.py --traffic-probe {key}")
     lines = [
         "# HBM traffic per call, every workload (rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE)", "",
@@ -379,7 +379,7 @@ def traffic_summary(d: str):
         "```",
         cmd.format(C="FETCH_SIZE", c="fetch", key="<key>"),
         cmd.format(C="WRITE_SIZE", c="write", key="<key>"),
-        "python3 bench.py --traffic-summary gpurun_out/traffic",
+        "python3 bench.py --traffic-summary <out>",
         "```", "",
         f"`<key>` is `copy` and each key below. Kernel sources hash: `{sha}`.", "",
         f"Scale: a plain {copy_bytes / 1e6:.0f} MB copy (`{ck}`) reads FETCH_SIZE = "
