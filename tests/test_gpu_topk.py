@@ -271,3 +271,26 @@ def test_subnormal_values(dev, dtype):
         err = np.abs(to_host(vals).astype(np.float64) - v64)
         tiny = v64 < 2.0 ** -126
         assert (err[tiny] <= 1e-5 * v64[tiny] + 2.0 ** -149).all(), what
+
+
+def test_split_plan_stays_within_two_workgroups_per_cu(dev):
+    """The top-k plan splits a small batch of long rows into chunks (a
+    workgroup each) whose count keeps the grid within two workgroups per CU,
+    with at least two chunks a row and at most 512 / K (the merge's one
+    register batch); and the planned call agrees with the oracle."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    for N, V, K in ((10, 1_000_000, 5), (10, 4_000_000, 5), (20, 1_000_000, 10), (200, 200_000, 5),
+                    (300, 100_000, 5), (4, 1_000_000, 10), (64, 128_256, 50)):
+        kernel, S = osm.topk_plan(N, V, K)
+        print(f"plan N={N} V={V} K={K}: ({kernel}, {S})", flush=True)
+        assert kernel == osm.KERNEL_SPLIT, (N, V, K, kernel, S)
+        assert 2 <= S <= max(2, 2 * cus // N), (N, V, K, S, cus)
+        assert S <= V // 4096 and S * K <= 512, (N, V, K, S)
+        if 2 * cus // N >= 2:
+            assert N * S <= 2 * cus, (N, S, cus)
+    # one planned call, checked against the oracle
+    x = synth.logits(10, 1_000_000, sigma=3.0, seed=77, device=dev)
+    vals, idx = osm.softmax_topk(x, 5)
+    torch.cuda.synchronize()
+    v64, z64 = oracle.topk(to_host(x), 5, "f32")
+    assert_topk_equal(to_host(vals), to_host(idx), v64, z64, "planned split 10x1e6 K=5")
