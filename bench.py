@@ -33,6 +33,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -523,10 +524,30 @@ def kernel_stats_summary(d: str, out_name: str, command: str):
          "|---|---|---|---|---|---|"]
     for name, n, avg, mn, mx, pc in rows[:25]:
         L.append(f"| `{name}` | {n} | {avg:.2f} | {mn:.2f} | {mx:.2f} | {pc:.1f} |")
+    # The bench's timed steps: its two step kernels' dispatches after the
+    # warm-up ones (the table above averages every call, stand-alone
+    # comparisons included).
+    m_steps = re.search(r"--steps (\d+)", command)
+    m_warm = re.search(r"--warmup (\d+)", command)
+    if m_steps and m_warm and glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True):
+        steps, warm = int(m_steps.group(1)), int(m_warm.group(1))
+        trace = _trace_dispatches(d)
+        L += ["", f"Timed steps (dispatches {warm + 1} to {warm + steps} of each step kernel, "
+              "from the kernel trace; the bench's own figures are event-timed in its own run):",
+              "", "| step kernel | dispatches | average us |", "|---|---|---|"]
+        for prefix in STEP_KERNELS:
+            ts = [t for n, t in trace if n.startswith(prefix)][warm:warm + steps]
+            if ts:
+                name = next(n for n, _ in trace if n.startswith(prefix))
+                L.append(f"| `{name}` | {len(ts)} | {sum(ts) / len(ts) / 1e3:.2f} |")
     with open(os.path.join(ROOT, "profiles", out_name), "w") as f:
         f.write("\n".join(L) + "\n")
     log(f"wrote profiles/{out_name}")
 
+
+# The kernels of one bench step (name prefixes as the profiler reports them):
+# the online softmax of the 4000 x 32000 binary32 batch and its fused top-5.
+STEP_KERNELS = ("osm::softmax_rows<float, 2, 1024, 1024,", "osm::topk_fused<float, 1, 5, 0,")
 
 # Core counters of the fused top-k and of the projection kernels: a kernel
 # trace and two counter passes per probe (each pass its own process, within
