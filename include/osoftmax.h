@@ -39,6 +39,13 @@
  *    the end of the process: call osm_stream_release before destroying a
  *    stream that has used the library, so that a later stream given the same
  *    handle starts without a buffer.
+ *  - Graph capture: the row kernels allocate nothing; the split kernels
+ *    (small batches of long rows) allocate their stream's scratch on its
+ *    first use and when it must grow.  Under HIP graph capture, either call
+ *    once outside the capture on the same stream with the largest shape to
+ *    be captured (the buffer is then reused and nothing is allocated), or use
+ *    softmax_topk_ex_noalloc for the top-k: an allocation recorded into a
+ *    graph would leave the stream's buffer owned by the graph.
  */
 #ifndef OSOFTMAX_H
 #define OSOFTMAX_H

@@ -143,9 +143,10 @@ int acquire_scratch(DeviceState* ds, std::unique_lock<std::mutex>& lk, hipStream
 
 // A zeroed array of at least `count` 32-bit counters for work enqueued on
 // `stream`; the kernels that use it leave it zeroed.  A stream's array grows
-// by a stream-ordered allocation, cleared in stream order; once the table is
-// full, a call gets an array of its own (*temp = true) to free after its
-// launches.  Locking as acquire_scratch.
+// by a stream-ordered allocation, cleared in stream order by a fill kernel
+// (not a memset, so that a call captured into a graph records a kernel
+// node); once the table is full, a call gets an array of its own
+// (*temp = true) to free after its launches.  Locking as acquire_scratch.
 int acquire_counters(DeviceState* ds, std::unique_lock<std::mutex>& lk, hipStream_t stream,
                      size_t count, uint32_t** out, bool* temp) {
     if (!ds->pool_ok) return OSM_ENOMEM;
@@ -164,8 +165,10 @@ int acquire_counters(DeviceState* ds, std::unique_lock<std::mutex>& lk, hipStrea
         (void)hipGetLastError();
         return OSM_ENOMEM;
     }
-    if (hipMemsetAsync(p, 0, want, stream) != hipSuccess) {
-        (void)hipGetLastError();
+    const int64_t words = (int64_t)(want / 4);
+    hipLaunchKernelGGL(zero_u32, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, stream,
+                       static_cast<uint32_t*>(p), words);
+    if (hipGetLastError() != hipSuccess) {
         (void)hipFreeAsync(p, stream);
         return OSM_EHIP;
     }
