@@ -440,6 +440,7 @@ struct TopkSmem {
     uint64_t published[TK_BLOCK / 64];
     MD wmd[TK_BLOCK / 64];
     float wmx[TK_BLOCK / 64];
+    int wq[TK_BLOCK / 64];  // keys queued after the list, per wavefront, at the row's end
 };
 
 // One (virtual) row by the W wavefronts of this thread's row group: row vr,
@@ -745,7 +746,11 @@ __device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restric
         step(bt, ok, b0, true);
     }
     while (cn > 0) cv_drain();
-    tw.flush();
+    // A row shared by W > 1 wavefronts and K <= TK_ROUNDS_MAX: no final
+    // selection per wavefront; the row's first wavefront selects once over
+    // every wavefront's list and queue (each under one row of 64 slots, as a
+    // selection runs whenever a queue reaches its trigger).
+    if (W == 1 || K > TK_ROUNDS_MAX) tw.flush();
 
     // merge of the normalizer pairs: wavefront butterflies, then (W > 1)
     // a fixed-order merge of the row's wavefronts
@@ -758,7 +763,10 @@ __device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restric
     }
     uint64_t key = tw.mine;
     if constexpr (W > 1) {
-        if (lane == 0) wmd[wv] = md;
+        if (lane == 0) {
+            wmd[wv] = md;
+            sm.wq[wv] = K <= TK_ROUNDS_MAX ? tw.qcount : 0;
+        }
         __syncthreads();
         if (rw != 0) return false;
         const int w0 = wv;  // first wavefront of the row
@@ -767,7 +775,7 @@ __device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restric
         for (int w = 1; w < W; ++w) md = md_merge(md, wmd[w0 + w]);
         uint64_t e[W];
 #pragma unroll
-        for (int w = 0; w < W; ++w) e[w] = (lane < K) ? region[w0 + w][lane] : 0ull;
+        for (int w = 0; w < W; ++w) e[w] = (lane < K + sm.wq[w0 + w]) ? region[w0 + w][lane] : 0ull;
         int found;
         key = select_topk<W>(e, W, K, &found);
     }
