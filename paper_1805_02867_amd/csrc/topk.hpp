@@ -773,11 +773,25 @@ __device__ __forceinline__ bool topk_vrow(TopkSmem<T, U>& sm, const T* __restric
         md = wmd[w0];
 #pragma unroll
         for (int w = 1; w < W; ++w) md = md_merge(md, wmd[w0 + w]);
-        uint64_t e[W];
+        if (K <= TK_ROUNDS_MAX) {
+            uint64_t e[W];
 #pragma unroll
-        for (int w = 0; w < W; ++w) e[w] = (lane < K + sm.wq[w0 + w]) ? region[w0 + w][lane] : 0ull;
-        int found;
-        key = select_topk<W>(e, W, K, &found);
+            for (int w = 0; w < W; ++w)
+                e[w] = (lane < K + sm.wq[w0 + w]) ? region[w0 + w][lane] : 0ull;
+            int found;
+            key = select_topk<W>(e, W, K, &found);
+        } else {
+            // the wavefronts' lists are sorted (lane 0 largest, 0 past the K-th):
+            // each is merged into the running one by a lane reversal, a maximum
+            // per lane and the 6-stage bitonic merge, instead of K rounds
+            uint64_t cur = lane < K ? region[w0][lane] : 0ull;
+#pragma unroll
+            for (int w = 1; w < W; ++w) {
+                const uint64_t q = reverse_lanes(lane < K ? region[w0 + w][lane] : 0ull);
+                cur = bitonic_merge_desc(cur > q ? cur : q);
+            }
+            key = lane < K ? cur : 0ull;
+        }
     }
     if constexpr (PART) {
         if constexpr (COH) {
